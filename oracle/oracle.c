@@ -1,0 +1,196 @@
+/*
+ * CPU oracle for the fused embedding-pooling + All-to-All send layout.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no code, header or constant with the GPU path.
+ *
+ * What it computes (the plain definition the fused operator must reach):
+ *
+ *   Embedding pooling (Sec. III-A): one logical workgroup of the original
+ *   EmbeddingBag kernel produces one pooled output vector; for table t and
+ *   sample b the bag is the index run offsets[t*B+b] .. offsets[t*B+b+1] and
+ *   the output is the (optionally per-index weighted) sum of the indexed rows.
+ *   Accumulation is in fp64, in index order; fp32/fp16/bf16 widen exactly.
+ *
+ *   All-to-All placement (Sec. III-A, worked example): the global batch is
+ *   split into R equal contiguous parts, the first part going to destination
+ *   0; destination r receives an array of shape {local batch S = B/R,
+ *   numTables x D} in which table t occupies the column range
+ *   [off_t, off_t + D_t) with off_t = sum of D over the tables before t.
+ *   So pooled vector (t, b) lands at send[r][s][off_t + j] with r = b / S,
+ *   s = b mod S.
+ *
+ *   Ready flags (Sec. III-A, "Book-keeping Flags"): one flag per slice; a
+ *   slice here is C consecutive samples of one destination for all tables, so
+ *   destination r has S / C slices and flag (r, c) is at r * (S / C) + c.
+ *   After `epoch` complete forwards from a zeroed array every flag equals
+ *   `epoch`.
+ *
+ * Readings of points the paper leaves open: empty bags give zeros; repeated
+ * indices count with multiplicity; out-of-range indices, non-monotone offsets,
+ * B % R != 0 and S % C != 0 are rejected; output is fp32 for every storage
+ * type, obtained by rounding the fp64 sum to nearest-even.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { OR_F32 = 0, OR_F16 = 1, OR_BF16 = 2 };
+
+enum {
+  OR_OK = 0,
+  OR_BAD_ARGS = -1,
+  OR_BAD_SPLIT = -2,    /* B % R != 0 or (B / R) % C != 0 */
+  OR_BAD_OFFSETS = -3,  /* offsets[0] != 0, decreasing, or last != nnz */
+  OR_BAD_INDEX = -4     /* index outside [0, rows_t) */
+};
+
+/* fp16 bit pattern -> exact double (IEEE 754 binary16: 1 sign, 5 exponent
+ * bits with bias 15, 10 fraction bits; exponent 0 is subnormal). */
+double oracle_half_to_double(uint16_t h) {
+  int sign = (h >> 15) & 1;
+  int e = (h >> 10) & 0x1f;
+  int f = h & 0x3ff;
+  double v;
+  if (e == 0)
+    v = ldexp((double)f, -24); /* f * 2^-10 * 2^-14 */
+  else if (e == 31)
+    v = f ? NAN : INFINITY;
+  else
+    v = ldexp((double)(f + 1024), e - 25); /* (1 + f/1024) * 2^(e-15) */
+  return sign ? -v : v;
+}
+
+/* bf16 bit pattern -> exact double: bf16 is the upper half of an fp32. */
+double oracle_bf16_to_double(uint16_t h) {
+  uint32_t bits = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &bits, sizeof f);
+  return (double)f;
+}
+
+static double load_elem(const void* table, int dtype, int64_t e) {
+  if (dtype == OR_F32) return (double)((const float*)table)[e];
+  if (dtype == OR_F16) return oracle_half_to_double(((const uint16_t*)table)[e]);
+  return oracle_bf16_to_double(((const uint16_t*)table)[e]);
+}
+
+/* Step 1: validate the inputs the way the definition needs them. */
+int oracle_validate(int32_t T, const int64_t* rows, const int32_t* dims, const int32_t* indices, int64_t nnz,
+                    const int64_t* offsets, int64_t B, int32_t R, int32_t C) {
+  if (T <= 0 || B <= 0 || R <= 0 || C <= 0 || !rows || !dims || !offsets || (nnz > 0 && !indices))
+    return OR_BAD_ARGS;
+  for (int32_t t = 0; t < T; ++t)
+    if (rows[t] < 0 || dims[t] <= 0) return OR_BAD_ARGS;
+  if (B % R != 0) return OR_BAD_SPLIT;
+  if ((B / R) % C != 0) return OR_BAD_SPLIT;
+  if (offsets[0] != 0 || offsets[(int64_t)T * B] != nnz) return OR_BAD_OFFSETS;
+  for (int64_t q = 0; q < (int64_t)T * B; ++q)
+    if (offsets[q + 1] < offsets[q]) return OR_BAD_OFFSETS;
+  for (int32_t t = 0; t < T; ++t)
+    for (int64_t k = offsets[(int64_t)t * B]; k < offsets[(int64_t)(t + 1) * B]; ++k)
+      if (indices[k] < 0 || (int64_t)indices[k] >= rows[t]) return OR_BAD_INDEX;
+  return OR_OK;
+}
+
+typedef struct {
+  int32_t T;
+  const void* const* tables;
+  const int32_t* dims;
+  const int64_t* col_off;
+  int64_t sum_dim;
+  int32_t dtype;
+  const int32_t* indices;
+  const int64_t* offsets;
+  const float* weights;
+  int64_t B;
+  int32_t R;
+  double* sum64;
+  double* abs64;
+  float* send;
+  int64_t b_begin, b_end;
+} job_t;
+
+/* Steps 2 and 3 for the samples [b_begin, b_end): pool every bag of those
+ * samples in fp64 and place it in the destination-partitioned layout. */
+static void* pool_range(void* arg) {
+  const job_t* J = (const job_t*)arg;
+  const int64_t S = J->B / J->R;
+  for (int64_t b = J->b_begin; b < J->b_end; ++b) {
+    const int64_t r = b / S;      /* destination rank: first S samples go to rank 0 */
+    const int64_t s = b % S;      /* row inside the destination's local batch */
+    for (int32_t t = 0; t < J->T; ++t) {
+      const int64_t D = J->dims[t];
+      const int64_t lo = J->offsets[(int64_t)t * J->B + b];
+      const int64_t hi = J->offsets[(int64_t)t * J->B + b + 1];
+      const int64_t out = (r * S + s) * J->sum_dim + J->col_off[t];
+      for (int64_t j = 0; j < D; ++j) {
+        double sum = 0.0, mag = 0.0;
+        for (int64_t k = lo; k < hi; ++k) {
+          const double w = J->weights ? (double)J->weights[k] : 1.0;
+          const double term = w * load_elem(J->tables[t], J->dtype, (int64_t)J->indices[k] * D + j);
+          sum += term;
+          mag += fabs(term);
+        }
+        if (J->sum64) J->sum64[out + j] = sum;
+        if (J->abs64) J->abs64[out + j] = mag;
+        if (J->send) J->send[out + j] = (float)sum;
+      }
+    }
+  }
+  return NULL;
+}
+
+/*
+ * Full pooled send buffer for one forward.
+ *   tables   : T host pointers, table t is rows[t] x dims[t], row-major, dtype
+ *   indices  : int32 [nnz], table-major CSR; offsets: int64 [T*B + 1]
+ *   weights  : fp32 [nnz] or NULL (plain sum)
+ *   sum64/abs64 : [B * sum(D)] fp64 (either may be NULL); send: fp32 [B * sum(D)]
+ *   nthreads : worker threads over sample ranges (<= 0 means 1)
+ * Returns OR_OK or a negative OR_* code (outputs untouched on error).
+ */
+int oracle_pool(int32_t T, const void* const* tables, const int64_t* rows, const int32_t* dims, int32_t dtype,
+                const int32_t* indices, int64_t nnz, const int64_t* offsets, const float* weights, int64_t B,
+                int32_t R, int32_t C, double* sum64, double* abs64, float* send, int32_t nthreads) {
+  if (!tables || dtype < OR_F32 || dtype > OR_BF16) return OR_BAD_ARGS;
+  int rc = oracle_validate(T, rows, dims, indices, nnz, offsets, B, R, C);
+  if (rc != OR_OK) return rc;
+  int64_t* col_off = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
+  if (!col_off) return OR_BAD_ARGS;
+  int64_t sum_dim = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    col_off[t] = sum_dim;
+    sum_dim += dims[t];
+  }
+  if (nthreads <= 0) nthreads = 1;
+  if (nthreads > B) nthreads = (int32_t)B;
+  job_t* jobs = (job_t*)calloc((size_t)nthreads, sizeof(job_t));
+  pthread_t* th = (pthread_t*)calloc((size_t)nthreads, sizeof(pthread_t));
+  for (int32_t i = 0; i < nthreads; ++i) {
+    job_t J = {T, tables, dims, col_off, sum_dim, dtype, indices, offsets, weights, B, R, sum64, abs64, send,
+               B * i / nthreads, B * (i + 1) / nthreads};
+    jobs[i] = J;
+  }
+  for (int32_t i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, pool_range, &jobs[i]);
+  pool_range(&jobs[0]);
+  for (int32_t i = 1; i < nthreads; ++i) pthread_join(th[i], NULL);
+  free(th);
+  free(jobs);
+  free(col_off);
+  return OR_OK;
+}
+
+/* Step 4: the ready flags after `epoch` complete forwards: R * (S / C)
+ * entries, slice (r, c) at r * (S / C) + c, each equal to epoch. */
+int oracle_flags(int64_t B, int32_t R, int32_t C, uint32_t epoch, uint32_t* flags, int64_t n_flags) {
+  if (B <= 0 || R <= 0 || C <= 0 || B % R || (B / R) % C) return OR_BAD_SPLIT;
+  const int64_t S = B / R, nC = S / C;
+  if (n_flags != R * nC || !flags) return OR_BAD_ARGS;
+  for (int64_t r = 0; r < R; ++r)
+    for (int64_t c = 0; c < nC; ++c) flags[r * nC + c] = epoch;
+  return OR_OK;
+}

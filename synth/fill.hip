@@ -1,0 +1,113 @@
+// Device side of the seeded input generator: fills a table in place with the
+// counter-based value function (SplitMix64, Steele/Lea/Flood 2014) so that
+// 10^11-byte tables never cross PCIe, and a plain 16-byte copy kernel used as
+// an HBM bandwidth probe and as the byte-counter calibration for profiling.
+//
+// The value function must match synth/gen.py bit for bit:
+//   u = splitmix64(seed ^ (row*dim + j)) >> 40
+//   uniform: v = float(int(u) - 2^23) * 2^-24 * 0.1f   (two separate RNE ops)
+//   cint:    v = float(int(u % 17) - 8)
+// followed by round-to-nearest-even to fp16 / bf16 storage.
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace {
+
+__device__ __forceinline__ uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ float value_of(uint64_t seed, uint64_t e, int kind) {
+  uint64_t u = splitmix64(seed ^ e) >> 40;
+  if (kind == 0) {
+    float x = (float)((int32_t)u - (1 << 23)) * 0x1p-24f;
+    return __fmul_rn(x, 0.1f);
+  }
+  return (float)((int32_t)(u % 17u) - 8);
+}
+
+__device__ __forceinline__ uint16_t bf16_rne(float v) {
+  uint32_t b = __float_as_uint(v);
+  return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+
+// One thread writes 8 consecutive elements (16 B for 16-bit, 32 B for fp32).
+__global__ void fill_kernel(void* dst, uint64_t n_elems, uint64_t seed, int kind, int dtype) {
+  uint64_t i0 = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8ull;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x * 8ull;
+  for (; i0 < n_elems; i0 += stride) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = value_of(seed, i0 + k, kind);
+    if (i0 + 8 <= n_elems) {
+      if (dtype == 0) {
+        float4* p = reinterpret_cast<float4*>(static_cast<float*>(dst) + i0);
+        p[0] = make_float4(v[0], v[1], v[2], v[3]);
+        p[1] = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          uint16_t lo, hi;
+          if (dtype == 1) {
+            lo = __half_as_ushort(__float2half_rn(v[2 * k]));
+            hi = __half_as_ushort(__float2half_rn(v[2 * k + 1]));
+          } else {
+            lo = bf16_rne(v[2 * k]);
+            hi = bf16_rne(v[2 * k + 1]);
+          }
+          w[k] = (uint32_t)lo | ((uint32_t)hi << 16);
+        }
+        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(dst) + i0) = make_uint4(w[0], w[1], w[2], w[3]);
+      }
+    } else {
+      for (int k = 0; i0 + k < n_elems; ++k) {
+        if (dtype == 0) static_cast<float*>(dst)[i0 + k] = v[k];
+        else if (dtype == 1) static_cast<__half*>(dst)[i0 + k] = __float2half_rn(v[k]);
+        else static_cast<uint16_t*>(dst)[i0 + k] = bf16_rne(v[k]);
+      }
+    }
+  }
+}
+
+__global__ void copy_kernel(uint4* __restrict__ dst, const uint4* __restrict__ src, uint64_t n16) {
+  uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (; i < n16; i += stride) dst[i] = src[i];
+}
+
+}  // namespace
+
+extern "C" {
+
+// Fill a rows x dim table with the counter-based values.  dtype 0 f32, 1 f16,
+// 2 bf16; kind 0 uniform(-0.05, 0.05), 1 integers in [-8, 8].  Returns 0 or
+// a hipError_t code.
+int synth_fill(void* dst, int64_t rows, int32_t dim, int32_t dtype, uint64_t seed, int32_t kind,
+               hipStream_t stream) {
+  if (!dst || rows < 0 || dim <= 0 || dtype < 0 || dtype > 2 || kind < 0 || kind > 1) return -1;
+  uint64_t n = (uint64_t)rows * (uint64_t)dim;
+  if (n == 0) return 0;
+  uint64_t threads = (n + 7) / 8;
+  uint64_t blocks = (threads + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(fill_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, dst, n, seed, kind, dtype);
+  return (int)hipGetLastError();
+}
+
+// dst[0:bytes) = src[0:bytes); bytes must be a multiple of 16 and both
+// pointers 16-byte aligned.  grid 0 = default.
+int synth_copy(void* dst, const void* src, int64_t bytes, int32_t grid, hipStream_t stream) {
+  if (!dst || !src || bytes < 0 || (bytes & 15) || ((uintptr_t)dst & 15) || ((uintptr_t)src & 15)) return -1;
+  uint64_t n16 = (uint64_t)bytes / 16;
+  if (n16 == 0) return 0;
+  unsigned g = grid > 0 ? (unsigned)grid : 4096u;
+  hipLaunchKernelGGL(copy_kernel, dim3(g), dim3(256), 0, stream, (uint4*)dst, (const uint4*)src, n16);
+  return (int)hipGetLastError();
+}
+
+}  // extern "C"

@@ -1,0 +1,43 @@
+"""Parser for the hand-worked fixture ``hand_example.txt``."""
+import os
+
+import numpy as np
+
+PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "hand_example.txt")
+
+
+def load(path=PATH):
+    d = {"tables": [], "sum": {}, "wsum": {}}
+    cur = None
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, *rest = line.split()
+            if key in ("T", "B", "R", "C"):
+                d[key] = int(rest[0])
+                cur = None
+            elif key == "table":
+                cur = []
+                d["tables"].append(cur)
+            elif key in ("offsets", "indices", "flags"):
+                d[key] = [int(x) for x in rest]
+                cur = None
+            elif key == "weights":
+                d[key] = [float(x) for x in rest]
+                cur = None
+            elif key in ("sum", "wsum"):
+                r, s, *vals = rest
+                d[key][(int(r), int(s))] = [float(x) for x in vals]
+                cur = None
+            else:
+                cur.append([float(x) for x in [key] + rest])
+    R, B = d["R"], d["B"]
+    S = B // R
+    for k in ("sum", "wsum"):
+        arr = np.zeros((R, S, len(next(iter(d[k].values())))))
+        for (r, s), v in d[k].items():
+            arr[r, s] = v
+        d[k] = arr
+    return d

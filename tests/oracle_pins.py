@@ -1,0 +1,268 @@
+"""Pins of the CPU oracle to facts fixed outside the oracle itself.
+
+Each ``pin_*`` takes a loaded oracle library (ctypes) and raises
+AssertionError when the oracle disagrees with:
+  * values worked out by hand (tests/golden/hand_example.txt),
+  * exact integer arithmetic (Python ints) on integer-valued tables,
+  * closed forms (all-ones tables, row-coded tables, single-row bags),
+  * a library routine on a special case (torch.nn.functional.embedding_bag),
+  * IEEE binary16 / bfloat16 decoding as done by numpy / torch,
+  * the placement rule of Sec. III-A (first B/R samples to destination 0,
+    {local batch, numTables x D} per destination, one flag per slice).
+The mutation test runs every pin against deliberately broken copies of the
+oracle and requires each copy to fail at least one pin.
+"""
+from __future__ import annotations
+
+import ctypes
+import fractions
+
+import numpy as np
+
+import oracle
+from tests.golden import hand
+
+
+def _pool(lib, tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=2):
+    return oracle.pool(tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=nthreads, lib=lib)
+
+
+def pin_hand(lib):
+    d = hand.load()
+    tabs = [np.array(t, dtype=np.float32) for t in d["tables"]]
+    dims = [t.shape[1] for t in tabs]
+    idx = np.array(d["indices"], dtype=np.int32)
+    off = np.array(d["offsets"], dtype=np.int64)
+    B, R, C = d["B"], d["R"], d["C"]
+    S = B // R
+    s64, a64, send = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C)
+    assert np.array_equal(send.reshape(R, S, -1), d["sum"].astype(np.float32)), "hand sum"
+    assert np.array_equal(s64.reshape(R, S, -1), d["sum"]), "hand sum64"
+    w = np.array(d["weights"], dtype=np.float32)
+    s64, a64, send = _pool(lib, tabs, 0, dims, idx, off, w, B, R, C)
+    assert np.array_equal(s64.reshape(R, S, -1), d["wsum"]), "hand weighted sum"
+    assert np.array_equal(send.reshape(R, S, -1), d["wsum"].astype(np.float32)), "hand weighted send"
+    fl = oracle.flags(B, R, C, 1, lib=lib)
+    assert fl.tolist() == d["flags"], "hand flags"
+
+
+def _random_bags(rng, T, B, rows, max_len, allow_empty=False):
+    lo = 0 if allow_empty else 1
+    lengths = rng.integers(lo, max_len + 1, size=T * B)
+    off = np.zeros(T * B + 1, dtype=np.int64)
+    off[1:] = np.cumsum(lengths)
+    idx = np.empty(off[-1], dtype=np.int32)
+    for t in range(T):
+        a, b = off[t * B], off[(t + 1) * B]
+        idx[a:b] = rng.integers(0, rows[t], size=b - a)
+    # force some repeated indices inside bags
+    for q in range(0, T * B, 7):
+        if off[q + 1] - off[q] >= 2:
+            idx[off[q] + 1] = idx[off[q]]
+    return off, idx
+
+
+def pin_integer_exact(lib):
+    """Integer-valued tables: sums are exact, so every correct order gives the
+    same bits; compare against Python integer arithmetic."""
+    rng = np.random.default_rng(11)
+    T, B, R, C = 3, 24, 4, 3
+    rows = [17, 40, 9]
+    dims = [4, 8, 12]
+    for dtype in (0, 1, 2):
+        ints = [rng.integers(-8, 9, size=(rows[t], dims[t])) for t in range(T)]
+        if dtype == 0:
+            tabs = [x.astype(np.float32) for x in ints]
+        elif dtype == 1:
+            tabs = [x.astype(np.float16) for x in ints]
+        else:
+            tabs = [(x.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16) for x in ints]
+        off, idx = _random_bags(rng, T, B, rows, 128, allow_empty=True)
+        s64, a64, send = _pool(lib, tabs, dtype, dims, idx, off, None, B, R, C)
+        col = 0
+        S = B // R
+        for t in range(T):
+            for b in range(B):
+                r, s = b // S, b % S
+                ks = range(off[t * B + b], off[t * B + b + 1])
+                exact = [sum(int(ints[t][idx[k]][j]) for k in ks) for j in range(dims[t])]
+                mags = [sum(abs(int(ints[t][idx[k]][j])) for k in ks) for j in range(dims[t])]
+                row = r * S + s
+                assert s64[row, col:col + dims[t]].tolist() == [float(v) for v in exact], (dtype, t, b)
+                assert a64[row, col:col + dims[t]].tolist() == [float(v) for v in mags], (dtype, t, b)
+                assert np.array_equal(send[row, col:col + dims[t]], np.array(exact, dtype=np.float32))
+            col += dims[t]
+
+
+def pin_ones_and_weights(lib):
+    """All-ones tables: plain sum = L, weighted sum = sum of weights (exact:
+    float32 U[0,1) weights are multiples of 2^-24, so the fp64 sum is exact)."""
+    rng = np.random.default_rng(5)
+    T, B, R, C = 2, 16, 2, 4
+    rows, dims = [30, 7], [8, 16]
+    tabs = [np.ones((rows[t], dims[t]), dtype=np.float32) for t in range(T)]
+    off, idx = _random_bags(rng, T, B, rows, 100, allow_empty=True)
+    w = rng.random(off[-1], dtype=np.float32)
+    s64, _, _ = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C)
+    s64w, a64w, _ = _pool(lib, tabs, 0, dims, idx, off, w, B, R, C)
+    col = 0
+    for t in range(T):
+        for b in range(B):
+            L = off[t * B + b + 1] - off[t * B + b]
+            assert np.all(s64[b, col:col + dims[t]] == L)
+            exact = sum(fractions.Fraction(float(x)) for x in w[off[t * B + b]:off[t * B + b + 1]])
+            assert np.all(s64w[b, col:col + dims[t]] == float(exact))
+            assert np.all(a64w[b, col:col + dims[t]] == float(exact))
+        col += dims[t]
+
+
+def pin_row_coded(lib):
+    """table_t[r][j] = r + 4096 t  =>  bag sum = sum(indices) + L * 4096 t
+    (exact: every bag sum stays below 2^24)."""
+    rng = np.random.default_rng(7)
+    T, B, R, C = 4, 32, 2, 8
+    N, D = 1000, 8
+    tabs = [np.repeat((np.arange(N) + 4096 * t).astype(np.float32)[:, None], D, axis=1) for t in range(T)]
+    off, idx = _random_bags(rng, T, B, [N] * T, 8)
+    _, _, send = _pool(lib, tabs, 0, [D] * T, idx, off, None, B, R, C)
+    for t in range(T):
+        for b in range(B):
+            ks = slice(off[t * B + b], off[t * B + b + 1])
+            L = off[t * B + b + 1] - off[t * B + b]
+            want = int(idx[ks].astype(np.int64).sum()) + L * 4096 * t
+            assert np.all(send[b, t * D:(t + 1) * D] == want), (t, b)
+
+
+def pin_placement(lib):
+    """Single-row bags on tables whose element (t, r, j) stores the code
+    (t * N + r) * D + j: every output element names its source, so the
+    placement send[r][s][off_t + j], b = r * S + s, is checked element by
+    element.  Also the worked example's shape (B = 4, two destinations, four
+    tables, slices of two samples)."""
+    for (T, N, dims, B, R, C) in [(3, 50, [4, 8, 12], 12, 3, 2), (4, 16, [4, 4, 4, 4], 4, 2, 2)]:
+        D_max = max(dims)
+        tabs = []
+        for t in range(T):
+            rr = np.arange(N)[:, None]
+            jj = np.arange(dims[t])[None, :]
+            tabs.append(((t * N + rr) * D_max + jj).astype(np.float32))
+        rng = np.random.default_rng(T)
+        off = np.arange(T * B + 1, dtype=np.int64)
+        idx = rng.integers(0, N, size=T * B).astype(np.int32)
+        _, _, send = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C)
+        S = B // R
+        view = send.reshape(R, S, sum(dims))
+        col = 0
+        for t in range(T):
+            for b in range(B):
+                r, s = b // S, b % S
+                got = view[r, s, col:col + dims[t]].astype(np.int64)
+                src_t, rem = divmod(got // D_max, N)
+                assert np.all(src_t == t) and np.all(rem == idx[t * B + b]), (t, b)
+                assert np.array_equal(got % D_max, np.arange(dims[t])), (t, b)
+            col += dims[t]
+        fl = oracle.flags(B, R, C, 3, lib=lib)
+        assert fl.size == R * (S // C) and np.all(fl == 3)
+
+
+def pin_fp16_decode(lib):
+    """All 65536 binary16 patterns decode exactly as numpy's float16 does."""
+    pats = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    want = pats.view(np.float16).astype(np.float64)
+    f = lib.oracle_half_to_double
+    got = np.array([f(int(p)) for p in pats])
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], want[~nan])
+
+
+def pin_bf16_decode(lib):
+    """All 65536 bfloat16 patterns decode exactly as torch's bfloat16 does."""
+    import torch
+    pats = np.arange(65536, dtype=np.int64)
+    want = torch.from_numpy(pats.astype(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    f = lib.oracle_bf16_to_double
+    got = np.array([f(int(p)) for p in pats])
+    nan = np.isnan(want)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], want[~nan])
+
+
+def pin_fp16_pool(lib):
+    """fp16 tables with subnormal and extreme values: pooled sums equal the
+    numpy-decoded fp64 sums of the same rows (single-row and multi-row bags)."""
+    rng = np.random.default_rng(3)
+    pats = np.array([0x0001, 0x03FF, 0x0400, 0x3C00, 0xBC00, 0x7BFF, 0xFBFF, 0x8001, 0x3555], dtype=np.uint16)
+    N, D, T, B, R, C = 9, 8, 1, 6, 1, 2
+    tab = rng.choice(pats, size=(N, D)).view(np.float16)
+    off = np.array([0, 1, 3, 6, 7, 9, 12], dtype=np.int64)
+    idx = rng.integers(0, N, size=12).astype(np.int32)
+    s64, _, _ = _pool(lib, [tab], 1, [D], idx, off, None, B, R, C)
+    for b in range(B):
+        want = np.zeros(D)
+        for k in range(off[b], off[b + 1]):
+            want = want + tab[idx[k]].astype(np.float64)
+        assert np.array_equal(s64[b], want)
+
+
+def pin_torch_embedding_bag(lib):
+    """Special case that reduces to a library routine: per table,
+    F.embedding_bag(mode='sum', per_sample_weights=w) in fp64, concatenated
+    along the feature axis, is the [B][sum D] send buffer."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(13)
+    T, B, R, C = 3, 40, 4, 5
+    rows, dims = [100, 37, 64], [16, 8, 32]
+    tabs = [rng.standard_normal((rows[t], dims[t])).astype(np.float32) for t in range(T)]
+    off, idx = _random_bags(rng, T, B, rows, 50)
+    w = rng.random(off[-1], dtype=np.float32)
+    for weights in (None, w):
+        s64, _, send = _pool(lib, tabs, 0, dims, idx, off, weights, B, R, C)
+        parts = []
+        for t in range(T):
+            a, b = off[t * B], off[(t + 1) * B]
+            inp = torch.from_numpy(idx[a:b].astype(np.int64))
+            offs = torch.from_numpy((off[t * B:(t + 1) * B] - a).astype(np.int64))
+            psw = None if weights is None else torch.from_numpy(weights[a:b].astype(np.float64))
+            parts.append(F.embedding_bag(inp, torch.from_numpy(tabs[t].astype(np.float64)), offs,
+                                         mode="sum", per_sample_weights=psw).numpy())
+        ref = np.concatenate(parts, axis=1)
+        assert np.allclose(s64, ref, rtol=1e-12, atol=1e-12)
+        # fp32 output is the fp64 sum rounded to nearest: within half an ulp
+        assert np.all(np.abs(send.astype(np.float64) - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12)
+
+
+def pin_validation(lib):
+    """Inputs outside the definition are rejected with the documented code."""
+    tabs = [np.zeros((4, 4), dtype=np.float32)]
+    off = np.array([0, 1, 2, 3, 4], dtype=np.int64)
+    idx = np.array([0, 1, 2, 3], dtype=np.int32)
+    cases = [
+        (dict(B=4, R=3, C=1), "B % R"),
+        (dict(B=4, R=2, C=3), "S % C"),
+    ]
+    for kw, _ in cases:
+        try:
+            _pool(lib, tabs, 0, [4], idx, off, None, **kw)
+        except oracle.OracleError as e:
+            assert "not zero" in str(e)
+        else:
+            raise AssertionError(kw)
+    for bad_off, bad_idx, msg in [
+        (np.array([0, 2, 1, 3, 4]), idx, "bad offsets"),
+        (np.array([1, 1, 2, 3, 4]), idx, "bad offsets"),
+        (np.array([0, 1, 2, 3, 3]), idx, "bad offsets"),
+        (off, np.array([0, 1, 4, 3]), "index out of range"),
+        (off, np.array([0, -1, 2, 3]), "index out of range"),
+    ]:
+        try:
+            _pool(lib, tabs, 0, [4], bad_idx, bad_off, None, 4, 2, 1)
+        except oracle.OracleError as e:
+            assert msg in str(e), (msg, e)
+        else:
+            raise AssertionError(msg)
+
+
+ALL_PINS = [pin_hand, pin_integer_exact, pin_ones_and_weights, pin_row_coded, pin_placement,
+            pin_fp16_decode, pin_bf16_decode, pin_fp16_pool, pin_torch_embedding_bag, pin_validation]
