@@ -1,0 +1,319 @@
+"""Benchmark of the fused embedding-bag pooling + All-to-All send layout.
+
+One step = one fused forward over one batch of the workload: pool every bag
+(gather L rows, sum or weighted-sum in fp32), store each pooled vector at its
+destination slot of the [R][B/R][sum D] send buffer and release the
+per-(destination, slice) ready flags.  Inputs are resident in HBM before the
+timed region.  Prints one JSON line (the headline workload, or one per
+workload with --all).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload dlrm]
+                       [--all] [--no-cpu-baseline] [--profile]
+       python bench.py --summarize DIR     (rocprofv3 csv output -> text summary)
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public specification
+KERNEL_SOURCES = ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
+                  "paper_2305_06942_amd/csrc/repack_consume.hip"]
+PAPER_CONTEXT = ("the paper's fused embedding + All-to-All reduced execution time by 20% intra-node "
+                 "(4x MI210 over Infinity Fabric, 80 GB/s) and 31% inter-node (2x MI210 over InfiniBand, "
+                 "20 GB/s); context only, those numbers include real inter-GPU transport")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(w, lengths, weighted):
+    """Bytes the method itself must move for one forward: every gathered row,
+    every index (+ weight), the CSR offsets, the fp32 output and one flag per
+    slice."""
+    import numpy as np
+    L = lengths.reshape(w.T, w.B).sum(axis=1)  # indices per table
+    rows = int(sum(int(L[t]) * w.dims[t] * w.elt for t in range(w.T)))
+    nnz = int(L.sum())
+    return rows + 4 * nnz + (4 * nnz if weighted else 0) + 8 * (w.T * w.B + 1) + 4 * w.B * w.sum_dim + 4 * w.n_chunks
+
+
+def traffic_record(workload):
+    """HBM bytes per launch from committed rocprofv3 counter runs, only if the
+    kernel sources have not changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_hash") != kernel_hash():
+        return None
+    return rec
+
+
+def time_launches(fn, steps, stream):
+    import torch
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(steps):
+        fn()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps  # ms per launch sequence
+
+
+def hbm_probe(nbytes=4 << 30, reps=10):
+    """Achievable copy bandwidth (read + write bytes / time) with a 16-byte
+    vector copy kernel."""
+    import torch
+    from synth import device as sdev
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    s = torch.cuda.current_stream()
+    sdev.copy(dst, src, nbytes)
+    ms = time_launches(lambda: sdev.copy(dst, src, nbytes), reps, s)
+    del src, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9, ms
+
+
+def cpu_baseline(w, inp, bytes_fn, max_tables=None):
+    """The CPU oracle timed on this host's cores over the first tables of the
+    same workload (all B samples of each)."""
+    import numpy as np
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    T = w.T if max_tables is None else min(w.T, max_tables)
+    try:
+        avail = int([l for l in open("/proc/meminfo") if l.startswith("MemAvailable")][0].split()[1]) * 1024
+    except Exception:
+        avail = 0
+    per_table = w.table_bytes() / w.T
+    while T > 1 and T * per_table * 2.5 > avail:
+        T //= 2
+    t0 = time.time()
+    tables = [inp.table(t) for t in range(T)]
+    gen_s = time.time() - t0
+    off = inp.offsets[:T * w.B + 1]
+    idx = inp.indices[:int(off[-1])]
+    wts = None if inp.weights is None else inp.weights[:int(off[-1])]
+    sub = w.with_(T=T, rows=w.rows[:T], dims=w.dims[:T])
+    nbytes = bytes_fn(sub, inp.lengths[:T * w.B], inp.weights is not None)
+    times = []
+    for _ in range(3):
+        t0 = time.time()
+        oracle.pool(tables, w.dtype, sub.dims, idx, off, wts, w.B, w.R, w.C, nthreads=cores,
+                    want_abs=False, want_sum=True, want_send=True)
+        times.append(time.time() - t0)
+    med = sorted(times)[1]
+    cpu_model = ""
+    try:
+        cpu_model = [l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name")][0]
+    except Exception:
+        pass
+    return {"value": round(nbytes / med / 1e9, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"C oracle (fp64) over tables 0..{T - 1} of {w.T}, all {w.B} samples "
+                      f"({nbytes / 1e9:.2f} GB algorithmic), median of 3 runs, {med:.3f} s each; "
+                      f"host tables generated in {gen_s:.1f} s (not timed); CPU {cpu_model}"}
+
+
+def run_workload(name, steps, warmup, with_cpu, profile):
+    import numpy as np
+    import torch
+
+    import paper_2305_06942_amd as ebag
+    import synth
+    from synth import device as sdev
+
+    w = synth.FULL[name]
+    t0 = time.time()
+    inp = synth.make_inputs(w)
+    log(f"[{name}] inputs generated in {time.time() - t0:.1f} s (nnz={inp.nnz})")
+    dev = sdev.to_device(inp)
+    torch.cuda.synchronize()
+    alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None)
+    plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R)
+    send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
+    recv = torch.empty_like(send)
+    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    epoch = [0]
+    stream = torch.cuda.current_stream()
+
+    def fused():
+        plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+        epoch[0] += 1
+
+    def unfused():
+        plan.unfused_forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+        epoch[0] += 1
+
+    for _ in range(warmup):
+        fused()
+    fused_ms = time_launches(fused, steps, stream)
+    for _ in range(warmup):
+        unfused()
+    unfused_ms = time_launches(unfused, steps, stream)
+    log(f"[{name}] fused {fused_ms * 1e3:.1f} us  unfused {unfused_ms * 1e3:.1f} us")
+    assert np.all(flags.cpu().numpy().view(np.uint32) == epoch[0]), "flags do not match the number of forwards"
+
+    out = {
+        "metric": "fused pooled-gather GB/s (% HBM peak) + fused vs unfused us per batch",
+        "value": round(alg / (fused_ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(fused_ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {0: "f32", 1: "f16->f32", 2: "bf16->f32"}[w.dtype],
+        "data": "synthetic (seeded generator; shapes of the workload below)",
+        "config": {"workload": name, "tables": w.T, "rows": w.rows[0], "dims": sorted(set(w.dims)),
+                   "storage": {0: "f32", 1: "f16", 2: "bf16"}[w.dtype], "global_batch": w.B,
+                   "bag_lengths": w.lengths, "indices": w.indices, "weighted": w.weighted,
+                   "destinations": w.R, "slice_samples": w.C, "parallelism": "1 GPU, R logical destinations"},
+        "fused_us": round(fused_ms * 1e3, 2),
+        "unfused_us": round(unfused_ms * 1e3, 2),
+        "fused_speedup_vs_unfused": round(unfused_ms / fused_ms, 4),
+        "pct_hbm_peak": round(100 * alg / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+        "algorithmic_bytes": alg,
+    }
+    if profile:
+        return out
+    # end to end with the concurrent consumer (producer enqueued first)
+    prod, cons = torch.cuda.Stream(), torch.cuda.Stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev_p, ev_c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e2e = []
+    for it in range(warmup + steps):
+        prod.wait_stream(stream)
+        cons.wait_stream(stream)
+        ev0.record(prod)
+        cons.wait_event(ev0)
+        with torch.cuda.stream(prod):
+            plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+        epoch[0] += 1
+        with torch.cuda.stream(cons):
+            plan.consume(send, flags, recv, w.B, w.R, epoch[0])
+        ev_p.record(prod)
+        ev_c.record(cons)
+        torch.cuda.synchronize()
+        if it >= warmup:
+            e2e.append(max(ev0.elapsed_time(ev_p), ev0.elapsed_time(ev_c)))
+    st = plan.status_ex()
+    assert st == (0, -1, 0, -1), f"consumer status {st}"
+    assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), "consumer copy differs"
+    out["fused_plus_consumer_us"] = round(1e3 * sorted(e2e)[len(e2e) // 2], 2)
+    # overlap evidence from device timestamps
+    tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1)
+    prod.wait_stream(stream)
+    cons.wait_stream(stream)
+    with torch.cuda.stream(prod):
+        tplan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+    epoch[0] += 1
+    with torch.cuda.stream(cons):
+        tplan.consume(send, flags, recv, w.B, w.R, epoch[0])
+    torch.cuda.synchronize()
+    rel, drn, tpu = tplan.trace(w.n_chunks)
+    out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
+    out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
+    out["n_slices"] = w.n_chunks
+    rows_alg = int(sum(int(inp.lengths.reshape(w.T, w.B)[t].sum()) * w.dims[t] * w.elt for t in range(w.T)))
+    out["unique_row_gbs"] = round((alg - rows_alg + inp.unique_row_bytes()) / (fused_ms * 1e-3) / 1e9, 2)
+    probe, _ = hbm_probe()
+    out["hbm_copy_probe_gbs"] = round(probe, 1)
+    out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                       "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None}
+    tr = traffic_record(name)
+    if tr:
+        out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
+    out["paper_context"] = PAPER_CONTEXT
+    del dev, send, recv
+    torch.cuda.empty_cache()
+    if with_cpu:
+        log(f"[{name}] timing the CPU oracle")
+        out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes)
+    return out
+
+
+def summarize(d):
+    """Summarise rocprofv3 csv output under d: per-kernel dispatch count and
+    mean / median duration, and per-kernel mean counter values."""
+    import csv
+    import statistics
+    lines = []
+    for path in sorted(glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)):
+        per = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+                per.setdefault(r["Kernel_Name"], []).append(dur)
+        lines.append(f"# kernel trace: {os.path.relpath(path, d)}")
+        lines.append(f"{'kernel':60s} {'calls':>6s} {'mean_us':>10s} {'median_us':>10s} {'min_us':>10s}")
+        for k, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
+            lines.append(f"{k[:60]:60s} {len(v):6d} {statistics.mean(v):10.2f} {statistics.median(v):10.2f} "
+                         f"{min(v):10.2f}")
+    for path in sorted(glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)):
+        per = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                key = (r["Kernel_Name"], r["Counter_Name"])
+                per.setdefault(key, []).append(float(r["Counter_Value"]))
+        lines.append(f"# counters: {os.path.relpath(path, d)}")
+        lines.append(f"{'kernel':60s} {'counter':>12s} {'calls':>6s} {'mean':>14s} {'median':>14s}")
+        for (k, c), v in sorted(per.items()):
+            lines.append(f"{k[:60]:60s} {c:>12s} {len(v):6d} {statistics.mean(v):14.1f} {statistics.median(v):14.1f}")
+    return "\n".join(lines)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="dlrm")
+    ap.add_argument("--all", action="store_true", help="every workload, one JSON line each")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile", action="store_true", help="timing loops only (for rocprofv3 runs)")
+    ap.add_argument("--summarize", metavar="DIR")
+    a = ap.parse_args()
+    if a.summarize:
+        print(summarize(a.summarize))
+        return 0
+    if a.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
+              "are logical slices of one GPU's send buffer)", file=sys.stderr)
+        return 2
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+    names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
+    for n in names:
+        out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile)
+        print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,196 @@
+/*
+ * ebag_a2a.h -- fused embedding-bag pooling + All-to-All send layout for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Sec. III-A of "Optimizing Distributed ML Communication with
+ * Fused Computation-Collective Operations"): every pooled embedding vector is
+ * produced by one logical workgroup of an EmbeddingBag kernel and stored
+ * directly where the All-to-All must deliver it, i.e. in a destination-
+ * partitioned send buffer of shape [R][B/R][sum_t D_t], and each slice is
+ * announced with a ready flag as soon as its last contributor finishes, so a
+ * consumer can move finished slices while pooling is still running.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  T tables; table t has rows_t rows of D_t elements of the plan's storage
+ *  type, dense and row-major (row r starts at byte r * D_t * elt), 16-byte
+ *  aligned.  D_t * elt must be a multiple of 16 bytes.
+ *
+ *  Bags are table-major CSR: bag (t, b) for sample b in [0, B) is
+ *  indices[offsets[t*B + b] .. offsets[t*B + b + 1]); offsets has T*B + 1
+ *  int64 entries, offsets[0] == 0, non-decreasing; indices are int32 in
+ *  [0, rows_t).  An empty bag pools to a zero vector; repeated indices count
+ *  with multiplicity.  weights (optional) are fp32, one per index: the bag
+ *  value is sum_k w_k * row_k (plain sum when weights == NULL).
+ *
+ *  Destinations: the batch is split into R contiguous parts of S = B / R
+ *  samples, the first to destination 0 (Sec. III-A, worked example).  Pooled
+ *  vector (t, b) is written as fp32 to send_buf[r][s][off_t + j] with
+ *  r = b / S, s = b % S, off_t = sum of D over tables before t -- the
+ *  {local batch, numTables x D} shape handed to the next operator.  The
+ *  memory order is identical to a [B][sum D] array.
+ *
+ *  Slices ("chunks"): slice (r, c) is the C samples r*S + c*C ..
+ *  r*S + (c+1)*C - 1 of destination r for all T tables -- a contiguous block
+ *  of C * sum(D) floats.  flags has R * (S / C) uint32 entries, slice (r, c)
+ *  at r * (S / C) + c (equivalently the global slice g = b / C).
+ *
+ *  Flags are epochs: the caller zeroes the flag array once; every completed
+ *  forward adds exactly 1 to every flag of the batch with release semantics
+ *  at device (agent) scope, after all of that slice's data is stored.  After
+ *  n forwards every flag equals n.
+ *
+ *  Pointers named *_buf, tables, indices, offsets, weights and flags are
+ *  device pointers owned by the caller; the library never frees them.  All
+ *  device work is enqueued on the given HIP stream; calls return as soon as
+ *  the work is enqueued.  One forward (fused or unfused) may be in flight per
+ *  plan at a time: the plan's slice counters and unfused scratch are shared.
+ *
+ * Errors: every entry point returns EBAG_OK (0) or a negative code, checked
+ * before anything is enqueued; ebag_a2a_last_error() returns a message for
+ * the calling thread's most recent failure.  Preconditions that are not
+ * checked on the host (index range, offset monotonicity) are checked in the
+ * kernels when the plan was created with check_indices = 1; a bad bag is then
+ * skipped (pooled as zeros) and reported by ebag_a2a_status().
+ */
+#ifndef EBAG_A2A_H
+#define EBAG_A2A_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ebag_a2a_plan* ebag_a2a_t;
+
+typedef enum { EBAG_F32 = 0, EBAG_F16 = 1, EBAG_BF16 = 2 } ebag_dtype_t;
+
+enum {
+  EBAG_OK = 0,
+  EBAG_EINVAL = -1,       /* bad argument (null pointer, size, split, alignment) */
+  EBAG_EUNSUPPORTED = -2, /* valid but not supported by this build */
+  EBAG_EHIP = -3,         /* a HIP runtime call failed */
+  EBAG_ETIMEOUT = -4,     /* reported by ebag_a2a_status() */
+  EBAG_ENOMEM = -5,       /* device or host allocation failed */
+  EBAG_EBUSY = -6         /* reserved */
+};
+
+/* Tuning and debugging knobs; pass NULL to ebag_a2a_create for defaults, or
+ * fill with ebag_a2a_default_opts() and change fields. */
+typedef struct ebag_a2a_opts {
+  int32_t waves_per_wg;        /* wavefronts (64 lanes) per pooling workgroup, 1..16 (default 4) */
+  int32_t bags_per_run;        /* bags a workgroup pools before one slice-counter update (default 16) */
+  int32_t rows_in_flight;      /* 16-byte row loads each wave keeps in flight: 4, 8 or 16 (default 8) */
+  int32_t persistent_wgs_per_cu; /* 0: one workgroup per run; >0: persistent grid of that many WGs per CU */
+  int32_t release_mode;        /* slice release: 1 (default) device-scope stores + completion wait, 0 agent-scope release fence per run */
+  int32_t chunk_order;         /* 0: natural slice order; 1: slices of destination self_rank last */
+  int32_t self_rank;           /* the destination whose slices stay local (chunk_order == 1) */
+  int32_t trace;               /* 1: record a device timestamp at every slice release and drain */
+  int32_t check_indices;       /* 1: kernels check offsets/indices, skip and report bad bags */
+  int32_t debug_suppress_flag; /* >= 0: never publish this slice's flag (failure-path tests); -1 off */
+  int32_t consumer_wgs;        /* workgroups of the consumer kernel (default 64) */
+  int32_t reserved;
+  int64_t consume_timeout_us;  /* consumer gives up after this long (default 5,000,000 us) */
+} ebag_a2a_opts_t;
+
+/* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */
+int ebag_a2a_default_opts(ebag_a2a_opts_t* opts);
+
+/*
+ * Create a plan for T tables on the current HIP device.
+ *   rows_per_table[T], dim_per_table[T]: host arrays; rows >= 0 (< 2^31), D > 0,
+ *     D * elt % 16 == 0.
+ *   table_dtype: storage type shared by all tables; pooled output is fp32.
+ *   chunk_samples (C): samples per slice, > 0.
+ *   max_batch: largest B any forward will use (sizes the slice counters and
+ *     the unfused scratch of max_batch * sum(D) floats).
+ *   max_ranks: largest R any forward will use.
+ * Device memory owned by the plan: slice counters, unfused scratch, table
+ * descriptors, status word, trace buffers; released by ebag_a2a_destroy.
+ */
+int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per_table,
+                    const int32_t* dim_per_table, ebag_dtype_t table_dtype, int32_t chunk_samples,
+                    int64_t max_batch, int32_t max_ranks, const ebag_a2a_opts_t* opts);
+
+/*
+ * Fused forward (Sec. III-A): pool every bag, store each pooled vector
+ * straight into send_buf at its destination slot (zero-copy placement,
+ * Sec. III-B / IV-B), and release each slice's flag (+1) when the last of
+ * its C*T bags is stored.  Slices complete progressively in slice order.
+ *   tables: HOST array of T device pointers (16-byte aligned).
+ *   indices, offsets, weights: device arrays as described above.
+ *   B > 0, R > 0, B % R == 0, (B / R) % C == 0, B <= max_batch, R <= max_ranks.
+ *   send_buf: device fp32 [B * sum(D)], 16-byte aligned.  flags: device
+ *   uint32 [B / C].
+ */
+int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices, const int64_t* offsets,
+                     const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
+                     hipStream_t stream);
+
+/*
+ * Bulk-synchronous baseline with the same contract and result: a pooling
+ * kernel writes per-table outputs [T][B][D_t] to plan scratch, then a
+ * repack kernel copies them into the send layout and releases each slice's
+ * flag -- the pool -> repack -> collective sequence at kernel boundaries
+ * that the fused operator replaces (Sec. II-B, IV-A).
+ */
+int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices,
+                             const int64_t* offsets, const float* weights, int64_t B, int32_t R,
+                             float* send_buf, uint32_t* flags, hipStream_t stream);
+
+/*
+ * Receiver side (Sec. III-A, "Book-keeping Flags"): each consumer workgroup
+ * owns a distinct subset of slices, polls each slice's flag with acquire
+ * semantics until it reaches expected_epoch, then copies the slice from
+ * send_buf to recv_buf (same layout and size).  Meant to run on a second
+ * stream concurrently with a forward.  Enqueue it after the forward it
+ * waits for: streams may share a hardware queue, and a consumer queued ahead
+ * of its producer on the same queue can only time out.  Polling is bounded
+ * by the plan's consume_timeout_us; on timeout the kernel stops and records
+ * the first missing slice for ebag_a2a_status().
+ */
+int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags, float* recv_buf, int64_t B,
+                     int32_t R, uint32_t expected_epoch, hipStream_t stream);
+
+/*
+ * Synchronise the device and read the plan's status word.
+ *   timed_out: 1 if a consumer gave up waiting, else 0.
+ *   first_missing_flag: lowest slice index a consumer timed out on, else -1.
+ * Returns EBAG_OK, or EBAG_ETIMEOUT when timed_out is set.
+ */
+int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_flag);
+
+/*
+ * Extended status: out[0] timed_out, out[1] first missing slice (-1 none),
+ * out[2] slices whose flag was seen above the expected epoch (double
+ * publication), out[3] first bad bag t*B+b found by check_indices (-1 none).
+ */
+int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]);
+
+/* Zero the slice counters and the status word (after a timeout or an
+ * aborted sequence).  Synchronous. */
+int ebag_a2a_reset(ebag_a2a_t h);
+
+/*
+ * Copy the per-slice timestamps of the most recent traced forward/consume
+ * (plan created with trace = 1) to host arrays of n entries:
+ * release_ticks[g] when slice g's flag was released, drain_ticks[g] when a
+ * consumer finished copying it (0 = not recorded).  Ticks are the device's
+ * constant wall clock; *ticks_per_us receives its rate.  Synchronous.
+ */
+int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks, int64_t n,
+                   double* ticks_per_us);
+
+/* Release the plan's device memory.  NULL is ignored. */
+void ebag_a2a_destroy(ebag_a2a_t h);
+
+/* Message for the calling thread's most recent failing call ("" if none). */
+const char* ebag_a2a_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EBAG_A2A_H */

@@ -1,0 +1,193 @@
+"""ctypes binding of include/ebag_a2a.h (same names, argument marshalling only).
+
+Device buffers may be passed as torch tensors (their ``data_ptr()`` is used)
+or as integer device addresses.  The stream defaults to torch's current
+stream on the current device.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libebag_a2a.so")
+
+EBAG_F32, EBAG_F16, EBAG_BF16 = 0, 1, 2
+EBAG_OK, EBAG_EINVAL, EBAG_EUNSUPPORTED, EBAG_EHIP, EBAG_ETIMEOUT, EBAG_ENOMEM, EBAG_EBUSY = 0, -1, -2, -3, -4, -5, -6
+
+
+class Opts(ctypes.Structure):
+    _fields_ = [
+        ("waves_per_wg", ctypes.c_int32),
+        ("bags_per_run", ctypes.c_int32),
+        ("rows_in_flight", ctypes.c_int32),
+        ("persistent_wgs_per_cu", ctypes.c_int32),
+        ("release_mode", ctypes.c_int32),
+        ("chunk_order", ctypes.c_int32),
+        ("self_rank", ctypes.c_int32),
+        ("trace", ctypes.c_int32),
+        ("check_indices", ctypes.c_int32),
+        ("debug_suppress_flag", ctypes.c_int32),
+        ("consumer_wgs", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("consume_timeout_us", ctypes.c_int64),
+    ]
+
+
+class EbagError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"ebag_a2a error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_SIGS = {
+    "ebag_a2a_default_opts": ([_P], ctypes.c_int),
+    "ebag_a2a_create": ([_P, ctypes.c_int32, _P, _P, ctypes.c_int, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P],
+                        ctypes.c_int),
+    "ebag_a2a_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
+    "ebag_a2a_unfused_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
+    "ebag_a2a_consume": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, _P], ctypes.c_int),
+    "ebag_a2a_status": ([_P, _P, _P], ctypes.c_int),
+    "ebag_a2a_status_ex": ([_P, _P], ctypes.c_int),
+    "ebag_a2a_reset": ([_P], ctypes.c_int),
+    "ebag_a2a_trace": ([_P, _P, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "ebag_a2a_destroy": ([_P], None),
+    "ebag_a2a_last_error": ([], ctypes.c_char_p),
+}
+
+
+def symbols():
+    """Names of the C ABI entry points this binding expects."""
+    return list(_SIGS)
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"HIP library {path} not found: build it with `python __graft_entry__.py` "
+                           "(there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    for name, (args, res) in _SIGS.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def last_error() -> str:
+    return load().ebag_a2a_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != EBAG_OK:
+        raise EbagError(rc, last_error())
+
+
+def _addr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def default_opts() -> Opts:
+    o = Opts()
+    _check(load().ebag_a2a_default_opts(ctypes.byref(o)))
+    return o
+
+
+class Plan:
+    """A plan for T tables (``ebag_a2a_create``); methods mirror the C ABI."""
+
+    def __init__(self, rows: Sequence[int], dims: Sequence[int], dtype: int, chunk_samples: int, max_batch: int,
+                 max_ranks: int, **opts):
+        lib = load()
+        o = default_opts()
+        for k, v in opts.items():
+            if not hasattr(o, k):
+                raise TypeError(f"unknown option {k}")
+            setattr(o, k, int(v))
+        self.T = len(rows)
+        self.dims = [int(d) for d in dims]
+        self.C = int(chunk_samples)
+        self.opts = o
+        rows_a = (ctypes.c_int64 * self.T)(*[int(r) for r in rows])
+        dims_a = (ctypes.c_int32 * self.T)(*self.dims)
+        h = ctypes.c_void_p()
+        _check(lib.ebag_a2a_create(ctypes.byref(h), self.T, rows_a, dims_a, int(dtype), self.C, int(max_batch),
+                                   int(max_ranks), ctypes.byref(o)))
+        self._h = h
+        self._lib = lib
+        self._tab_cache = None
+
+    def _tables(self, tables):
+        ptrs = [_addr(t) for t in tables]
+        if len(ptrs) != self.T:
+            raise ValueError(f"expected {self.T} tables, got {len(ptrs)}")
+        if self._tab_cache is None or self._tab_cache[0] != ptrs:
+            self._tab_cache = (ptrs, (ctypes.c_void_p * self.T)(*ptrs))
+        return self._tab_cache[1]
+
+    def forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
+        _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
+                                          _addr(weights), int(B), int(R), _addr(send), _addr(flags), _stream(stream)))
+
+    def unfused_forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
+        _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
+                                                  _addr(weights), int(B), int(R), _addr(send), _addr(flags),
+                                                  _stream(stream)))
+
+    def consume(self, send, flags, recv, B, R, expected_epoch, stream=None):
+        _check(self._lib.ebag_a2a_consume(self._h, _addr(send), _addr(flags), _addr(recv), int(B), int(R),
+                                          int(expected_epoch) & 0xFFFFFFFF, _stream(stream)))
+
+    def status(self):
+        """(timed_out, first_missing_flag); synchronises the device."""
+        s = (ctypes.c_int32 * 4)()
+        _check(self._lib.ebag_a2a_status_ex(self._h, s))
+        return s[0], s[1]
+
+    def status_ex(self):
+        s = (ctypes.c_int32 * 4)()
+        _check(self._lib.ebag_a2a_status_ex(self._h, s))
+        return tuple(s)
+
+    def reset(self):
+        _check(self._lib.ebag_a2a_reset(self._h))
+
+    def trace(self, n):
+        import numpy as np
+        rel = np.zeros(n, dtype=np.uint64)
+        drn = np.zeros(n, dtype=np.uint64)
+        tpu = ctypes.c_double()
+        _check(self._lib.ebag_a2a_trace(self._h, rel.ctypes.data, drn.ctypes.data, n, ctypes.byref(tpu)))
+        return rel, drn, tpu.value
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.ebag_a2a_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,111 @@
+// Internal definitions shared by the host plan code and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ebag {
+
+// Per-table constants, resident in device memory for the plan's lifetime.
+struct TabMeta {
+  int64_t rows;      // number of rows
+  int64_t row_bytes; // D * elt (multiple of 16)
+  int32_t dim;       // D
+  int32_t col_off;   // first column of this table in a send-buffer row
+  int32_t vecs;      // 16-byte vectors per row (= row_bytes / 16)
+  int32_t vshift;    // log2(vecs) when vecs is a power of two <= 64, else -1
+};
+
+// Order in which slices are produced and drained.  order 0: natural; order
+// 1: slices of destination `self` last, so slices bound for other
+// destinations are finished (and can be shipped) first (Sec. III-A,
+// communication-aware scheduling).
+struct SliceOrder {
+  int64_t n_chunks;    // B / C
+  int64_t per_rank;    // (B / R) / C
+  int64_t self;        // destination kept local
+  int32_t order;
+  int32_t pad;
+};
+
+__host__ __device__ inline int64_t slice_at(const SliceOrder& o, int64_t x) {
+  if (o.order == 0) return x;
+  const int64_t lo = o.self * o.per_rank;
+  const int64_t others = o.n_chunks - o.per_rank;
+  if (x < lo) return x;
+  if (x < others) return x + o.per_rank;
+  return lo + (x - others);
+}
+
+struct PoolArgs {
+  const void* const* tables;  // [T] table base pointers
+  const TabMeta* meta;        // [T]
+  const int32_t* tperm;       // [T] position within a slice -> table
+  const int32_t* indices;
+  const int64_t* offsets;
+  const float* weights;       // nullptr for plain sum
+  float* out;                 // fused: send buffer; unfused: [T][B][D_t] scratch
+  uint32_t* counters;         // [n_chunks] bags finished per slice (self-resetting)
+  uint32_t* flags;            // [n_chunks] epoch flags
+  int32_t* status;            // plan status word
+  uint64_t* trace_release;    // [n_chunks] or nullptr
+  int64_t B;
+  int64_t nruns;
+  int64_t suppress;           // slice whose flag is never released (-1: none)
+  SliceOrder so;
+  int32_t T;
+  int32_t C;
+  int32_t K;                  // bags per run
+  int32_t J;                  // runs per (slice, table) = ceil(C / K)
+  int32_t sum_dim;
+  int32_t check;              // check offsets / indices
+  int32_t release_mode;       // 0 agent-scope release fence, 1 device-scope stores + completion wait
+  int32_t pad;
+};
+
+struct RepackArgs {
+  const float* scratch;       // [T][B][D_t]
+  float* send;                // [B][sum D]
+  const TabMeta* meta;
+  const int32_t* tperm;
+  int64_t B;
+  SliceOrder so;
+  int32_t T;
+  int32_t C;
+  int32_t sum_dim;
+  int32_t pad;
+};
+
+// Bulk-synchronous flag publication after the repack kernel.
+struct PublishArgs {
+  uint32_t* flags;
+  uint64_t* trace_release;
+  int64_t n_chunks;
+  int64_t suppress;
+};
+
+struct ConsumeArgs {
+  const float* send;
+  const uint32_t* flags;
+  float* recv;
+  int32_t* status;
+  uint64_t* trace_drain;
+  int64_t chunk_floats;       // C * sum D
+  uint64_t timeout_ticks;
+  SliceOrder so;
+  uint32_t epoch;
+  int32_t pad;
+};
+
+// Status word layout (int32[4]).
+enum { ST_TIMED_OUT = 0, ST_FIRST_MISSING = 1, ST_OVERSHOOT = 2, ST_FIRST_BAD_BAG = 3 };
+
+// Launchers (return hipError_t of the launch).
+hipError_t launch_pool(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, const PoolArgs& a,
+                       int grid, int block, hipStream_t stream);
+hipError_t launch_repack(const RepackArgs& a, int grid, int block, hipStream_t stream);
+hipError_t launch_publish(const PublishArgs& a, hipStream_t stream);
+hipError_t launch_consume(const ConsumeArgs& a, int grid, int block, hipStream_t stream);
+int pool_max_wgs_per_cu(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, int block);
+
+}  // namespace ebag

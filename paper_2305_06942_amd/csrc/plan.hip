@@ -1,0 +1,453 @@
+// Host side of the C ABI declared in include/ebag_a2a.h: argument checks,
+// plan-owned device memory, launch geometry and kernel dispatch.
+#include <climits>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ebag_a2a.h"
+#include "common.h"
+
+using namespace ebag;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(EBAG_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(call, what)              \
+  do {                                   \
+    hipError_t e_ = (call);              \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int log2_exact(int v) {
+  for (int s = 0; s <= 6; ++s)
+    if ((1 << s) == v) return s;
+  return -1;
+}
+
+}  // namespace
+
+struct ebag_a2a_plan {
+  int device = 0;
+  int32_t T = 0;
+  int dtype = 0;
+  int elt = 4;
+  int32_t C = 0;
+  int64_t max_batch = 0;
+  int32_t max_ranks = 0;
+  int32_t sum_dim = 0;
+  int num_cus = 0;
+  double ticks_per_us = 100.0;
+  ebag_a2a_opts_t opts{};
+  std::vector<TabMeta> meta;
+  std::vector<const void*> host_tables;  // last table pointers uploaded
+  bool tables_valid = false;
+  int64_t max_chunks = 0;
+  // device memory
+  TabMeta* d_meta = nullptr;
+  int32_t* d_tperm = nullptr;
+  const void** d_tables = nullptr;
+  uint32_t* d_counters = nullptr;
+  float* d_scratch = nullptr;
+  int32_t* d_status = nullptr;
+  uint64_t* d_trace_release = nullptr;
+  uint64_t* d_trace_drain = nullptr;
+};
+
+namespace {
+
+const int32_t kStatusInit[4] = {0, INT_MAX, 0, INT_MAX};
+
+void free_plan(ebag_a2a_plan* h) {
+  if (!h) return;
+  (void)hipFree(h->d_meta);
+  (void)hipFree(h->d_tperm);
+  (void)hipFree(h->d_tables);
+  (void)hipFree(h->d_counters);
+  (void)hipFree(h->d_scratch);
+  (void)hipFree(h->d_status);
+  (void)hipFree(h->d_trace_release);
+  (void)hipFree(h->d_trace_drain);
+  delete h;
+}
+
+int check_opts(const ebag_a2a_opts_t& o) {
+  if (o.waves_per_wg < 1 || o.waves_per_wg > 16) return fail(EBAG_EINVAL, "waves_per_wg must be in [1, 16]");
+  if (o.bags_per_run < 1) return fail(EBAG_EINVAL, "bags_per_run must be >= 1");
+  if (o.rows_in_flight != 4 && o.rows_in_flight != 8 && o.rows_in_flight != 16)
+    return fail(EBAG_EINVAL, "rows_in_flight must be 4, 8 or 16");
+  if (o.persistent_wgs_per_cu < -1) return fail(EBAG_EINVAL, "persistent_wgs_per_cu must be >= -1");
+  if (o.release_mode < 0 || o.release_mode > 1) return fail(EBAG_EINVAL, "release_mode must be 0 or 1");
+  if (o.chunk_order != 0 && o.chunk_order != 1) return fail(EBAG_EINVAL, "chunk_order must be 0 or 1");
+  if (o.self_rank < 0) return fail(EBAG_EINVAL, "self_rank must be >= 0");
+  if (o.consumer_wgs < 1) return fail(EBAG_EINVAL, "consumer_wgs must be >= 1");
+  if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
+  return EBAG_OK;
+}
+
+// Validation shared by both forwards; fills the slice order.
+int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32_t* indices, const int64_t* offsets,
+                  int64_t B, int32_t R, const float* send_buf, const uint32_t* flags, SliceOrder* so) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (!tables) return fail(EBAG_EINVAL, "null table pointer array");
+  if (!offsets || !send_buf || !flags) return fail(EBAG_EINVAL, "null offsets, send_buf or flags");
+  if (!indices) return fail(EBAG_EINVAL, "null indices");
+  if (B <= 0 || R <= 0) return fail(EBAG_EINVAL, "B and R must be positive (B=%lld R=%d)", (long long)B, R);
+  if (B > h->max_batch) return fail(EBAG_EINVAL, "B=%lld exceeds max_batch=%lld", (long long)B, (long long)h->max_batch);
+  if (R > h->max_ranks) return fail(EBAG_EINVAL, "R=%d exceeds max_ranks=%d", R, h->max_ranks);
+  if (B % R != 0) return fail(EBAG_EINVAL, "B=%lld is not a multiple of R=%d", (long long)B, R);
+  const int64_t S = B / R;
+  if (S % h->C != 0) return fail(EBAG_EINVAL, "B/R=%lld is not a multiple of chunk_samples=%d", (long long)S, h->C);
+  if (!aligned16(send_buf)) return fail(EBAG_EINVAL, "send_buf is not 16-byte aligned");
+  for (int32_t t = 0; t < h->T; ++t) {
+    if (!tables[t] && h->meta[t].rows > 0) return fail(EBAG_EINVAL, "null pointer for table %d", t);
+    if (!aligned16(tables[t])) return fail(EBAG_EINVAL, "table %d is not 16-byte aligned", t);
+  }
+  if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
+    return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
+  so->n_chunks = B / h->C;
+  so->per_rank = S / h->C;
+  so->self = h->opts.self_rank;
+  so->order = h->opts.chunk_order;
+  so->pad = 0;
+  return EBAG_OK;
+}
+
+// Upload table pointers when they differ from the last upload.  The copy is
+// ordered on `stream` and completed before returning, so the caller's host
+// array may be reused immediately.
+int sync_tables(ebag_a2a_plan* h, const void* const* tables, hipStream_t stream) {
+  if (h->tables_valid && std::memcmp(h->host_tables.data(), tables, sizeof(void*) * h->T) == 0) return EBAG_OK;
+  std::memcpy(h->host_tables.data(), tables, sizeof(void*) * h->T);
+  HIP_TRY(hipMemcpyAsync(h->d_tables, h->host_tables.data(), sizeof(void*) * h->T, hipMemcpyHostToDevice, stream),
+          "upload table pointers");
+  HIP_TRY(hipStreamSynchronize(stream), "upload table pointers");
+  h->tables_valid = true;
+  return EBAG_OK;
+}
+
+void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_t* offsets, const float* weights,
+                    int64_t B, const SliceOrder& so, float* out, uint32_t* flags, PoolArgs* a) {
+  std::memset(a, 0, sizeof *a);
+  const int32_t K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  a->tables = h->d_tables;
+  a->meta = h->d_meta;
+  a->tperm = h->d_tperm;
+  a->indices = indices;
+  a->offsets = offsets;
+  a->weights = weights;
+  a->out = out;
+  a->counters = h->d_counters;
+  a->flags = flags;
+  a->status = h->d_status;
+  a->trace_release = h->opts.trace ? h->d_trace_release : nullptr;
+  a->B = B;
+  a->K = K;
+  a->J = (h->C + K - 1) / K;
+  a->T = h->T;
+  a->C = h->C;
+  a->nruns = so.n_chunks * (int64_t)h->T * a->J;
+  a->suppress = h->opts.debug_suppress_flag;
+  a->so = so;
+  a->sum_dim = h->sum_dim;
+  a->check = h->opts.check_indices;
+  a->release_mode = h->opts.release_mode;
+}
+
+// The fast pooling kernels handle row widths of 2^k <= 64 sixteen-byte
+// vectors without index checks; anything else uses the checked kernels.
+bool needs_safe(const ebag_a2a_plan* h) {
+  if (h->opts.check_indices) return true;
+  for (const TabMeta& m : h->meta)
+    if (m.vshift < 0) return true;
+  return false;
+}
+
+int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, int block) {
+  int64_t grid = nruns;
+  if (h->opts.persistent_wgs_per_cu != 0) {
+    int per_cu = h->opts.persistent_wgs_per_cu;
+    if (per_cu < 0)
+      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, false, fused, needs_safe(h), block);
+    if (per_cu < 1) per_cu = 1;
+    const int64_t pg = (int64_t)per_cu * h->num_cus;
+    if (pg < grid) grid = pg;
+  }
+  if (grid > INT_MAX) grid = INT_MAX;
+  return (int)grid;
+}
+
+}  // namespace
+
+extern "C" {
+
+int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
+  if (!o) return fail(EBAG_EINVAL, "null opts");
+  std::memset(o, 0, sizeof *o);
+  o->waves_per_wg = 4;
+  o->bags_per_run = 16;
+  o->rows_in_flight = 8;
+  o->persistent_wgs_per_cu = 0;
+  o->release_mode = 1;
+  o->chunk_order = 0;
+  o->self_rank = 0;
+  o->trace = 0;
+  o->check_indices = 0;
+  o->debug_suppress_flag = -1;
+  o->consumer_wgs = 64;
+  o->consume_timeout_us = 5000000;
+  return EBAG_OK;
+}
+
+int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per_table,
+                    const int32_t* dim_per_table, ebag_dtype_t table_dtype, int32_t chunk_samples,
+                    int64_t max_batch, int32_t max_ranks, const ebag_a2a_opts_t* opts) {
+  if (!out) return fail(EBAG_EINVAL, "null output handle");
+  *out = nullptr;
+  if (num_tables <= 0) return fail(EBAG_EINVAL, "num_tables must be positive");
+  if (!rows_per_table || !dim_per_table) return fail(EBAG_EINVAL, "null rows/dims array");
+  if (table_dtype != EBAG_F32 && table_dtype != EBAG_F16 && table_dtype != EBAG_BF16)
+    return fail(EBAG_EINVAL, "unknown table dtype %d", (int)table_dtype);
+  if (chunk_samples <= 0) return fail(EBAG_EINVAL, "chunk_samples must be positive");
+  if (max_batch <= 0 || max_ranks <= 0) return fail(EBAG_EINVAL, "max_batch and max_ranks must be positive");
+  ebag_a2a_opts_t o;
+  if (opts)
+    o = *opts;
+  else
+    ebag_a2a_default_opts(&o);
+  int rc = check_opts(o);
+  if (rc) return rc;
+  const int elt = table_dtype == EBAG_F32 ? 4 : 2;
+  std::vector<TabMeta> meta(num_tables);
+  int64_t sum_dim = 0;
+  for (int32_t t = 0; t < num_tables; ++t) {
+    const int64_t rows = rows_per_table[t];
+    const int32_t D = dim_per_table[t];
+    if (rows < 0 || rows > INT32_MAX) return fail(EBAG_EINVAL, "rows of table %d out of range", t);
+    if (D <= 0) return fail(EBAG_EINVAL, "dim of table %d must be positive", t);
+    if (((int64_t)D * elt) % 16 != 0)
+      return fail(EBAG_EINVAL, "table %d: D*elt = %lld bytes is not a multiple of 16", t, (long long)D * elt);
+    meta[t].rows = rows;
+    meta[t].row_bytes = (int64_t)D * elt;
+    meta[t].dim = D;
+    meta[t].col_off = (int32_t)sum_dim;
+    meta[t].vecs = (int32_t)(meta[t].row_bytes / 16);
+    meta[t].vshift = log2_exact(meta[t].vecs);
+    sum_dim += D;
+  }
+  if (sum_dim > INT32_MAX / 4) return fail(EBAG_EINVAL, "sum of dims too large");
+  if ((int64_t)max_batch * sum_dim > (int64_t)1 << 40) return fail(EBAG_EINVAL, "max_batch * sum(D) too large");
+
+  ebag_a2a_plan* h = new (std::nothrow) ebag_a2a_plan();
+  if (!h) return fail(EBAG_ENOMEM, "host allocation failed");
+  h->T = num_tables;
+  h->dtype = (int)table_dtype;
+  h->elt = elt;
+  h->C = chunk_samples;
+  h->max_batch = max_batch;
+  h->max_ranks = max_ranks;
+  h->sum_dim = (int32_t)sum_dim;
+  h->opts = o;
+  h->meta = meta;
+  h->host_tables.assign(num_tables, nullptr);
+  h->max_chunks = (max_batch + chunk_samples - 1) / chunk_samples;
+
+#define CREATE_TRY(call, what)                                                             \
+  do {                                                                                     \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess) {                                                                \
+      int r_ = e_ == hipErrorOutOfMemory ? fail(EBAG_ENOMEM, "%s: out of device memory", what) \
+                                         : hip_fail(e_, what);                              \
+      free_plan(h);                                                                        \
+      return r_;                                                                           \
+    }                                                                                      \
+  } while (0)
+
+  CREATE_TRY(hipGetDevice(&h->device), "hipGetDevice");
+  CREATE_TRY(hipDeviceGetAttribute(&h->num_cus, hipDeviceAttributeMultiprocessorCount, h->device), "CU count");
+  int khz = 0;
+  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device) == hipSuccess && khz > 0)
+    h->ticks_per_us = khz / 1000.0;
+  std::vector<int32_t> tperm(num_tables);
+  for (int32_t t = 0; t < num_tables; ++t) tperm[t] = t;
+  CREATE_TRY(hipMalloc((void**)&h->d_meta, sizeof(TabMeta) * num_tables), "alloc table meta");
+  CREATE_TRY(hipMemcpy(h->d_meta, meta.data(), sizeof(TabMeta) * num_tables, hipMemcpyHostToDevice), "upload meta");
+  CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");
+  CREATE_TRY(hipMemcpy(h->d_tperm, tperm.data(), sizeof(int32_t) * num_tables, hipMemcpyHostToDevice), "upload order");
+  CREATE_TRY(hipMalloc((void**)&h->d_tables, sizeof(void*) * num_tables), "alloc table pointers");
+  CREATE_TRY(hipMalloc((void**)&h->d_counters, sizeof(uint32_t) * h->max_chunks), "alloc slice counters");
+  CREATE_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_chunks), "zero slice counters");
+  CREATE_TRY(hipMalloc((void**)&h->d_scratch, sizeof(float) * (size_t)max_batch * (size_t)sum_dim), "alloc scratch");
+  CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
+  CREATE_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "init status");
+  if (o.trace) {
+    CREATE_TRY(hipMalloc((void**)&h->d_trace_release, sizeof(uint64_t) * h->max_chunks), "alloc trace");
+    CREATE_TRY(hipMalloc((void**)&h->d_trace_drain, sizeof(uint64_t) * h->max_chunks), "alloc trace");
+    CREATE_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+    CREATE_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+  }
+#undef CREATE_TRY
+  *out = h;
+  g_err.clear();
+  return EBAG_OK;
+}
+
+int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices, const int64_t* offsets,
+                     const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
+                     hipStream_t stream) {
+  SliceOrder so;
+  int rc = check_forward(h, tables, indices, offsets, B, R, send_buf, flags, &so);
+  if (rc) return rc;
+  rc = sync_tables(h, tables, stream);
+  if (rc) return rc;
+  PoolArgs a;
+  fill_pool_args(h, indices, offsets, weights, B, so, send_buf, flags, &a);
+  const int block = 64 * h->opts.waves_per_wg;
+  const int grid = pool_grid(h, a.nruns, true, block);
+  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(h), a, grid,
+                             block, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
+  return EBAG_OK;
+}
+
+int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices,
+                             const int64_t* offsets, const float* weights, int64_t B, int32_t R,
+                             float* send_buf, uint32_t* flags, hipStream_t stream) {
+  SliceOrder so;
+  int rc = check_forward(h, tables, indices, offsets, B, R, send_buf, flags, &so);
+  if (rc) return rc;
+  rc = sync_tables(h, tables, stream);
+  if (rc) return rc;
+  PoolArgs a;
+  fill_pool_args(h, indices, offsets, weights, B, so, h->d_scratch, flags, &a);
+  const int block = 64 * h->opts.waves_per_wg;
+  const int grid = pool_grid(h, a.nruns, false, block);
+  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(h), a, grid,
+                             block, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch pooling kernel");
+  RepackArgs r;
+  std::memset(&r, 0, sizeof r);
+  r.scratch = h->d_scratch;
+  r.send = send_buf;
+  r.meta = h->d_meta;
+  r.tperm = h->d_tperm;
+  r.B = B;
+  r.so = so;
+  r.T = h->T;
+  r.C = h->C;
+  r.sum_dim = h->sum_dim;
+  const int64_t rgrid = so.n_chunks * h->T;
+  if (rgrid > INT_MAX) return fail(EBAG_EINVAL, "too many slices x tables for the repack grid");
+  e = launch_repack(r, (int)rgrid, 256, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch repack kernel");
+  PublishArgs pa;
+  pa.flags = flags;
+  pa.trace_release = h->opts.trace ? h->d_trace_release : nullptr;
+  pa.n_chunks = so.n_chunks;
+  pa.suppress = h->opts.debug_suppress_flag;
+  e = launch_publish(pa, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch flag publication kernel");
+  return EBAG_OK;
+}
+
+int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags, float* recv_buf, int64_t B,
+                     int32_t R, uint32_t expected_epoch, hipStream_t stream) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (!send_buf || !flags || !recv_buf) return fail(EBAG_EINVAL, "null send_buf, flags or recv_buf");
+  if (!aligned16(send_buf) || !aligned16(recv_buf)) return fail(EBAG_EINVAL, "send/recv not 16-byte aligned");
+  if (B <= 0 || R <= 0 || B > h->max_batch || R > h->max_ranks || B % R || (B / R) % h->C)
+    return fail(EBAG_EINVAL, "bad B=%lld / R=%d for this plan", (long long)B, R);
+  if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
+    return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
+  ConsumeArgs c;
+  std::memset(&c, 0, sizeof c);
+  c.send = send_buf;
+  c.flags = flags;
+  c.recv = recv_buf;
+  c.status = h->d_status;
+  c.trace_drain = h->opts.trace ? h->d_trace_drain : nullptr;
+  c.chunk_floats = (int64_t)h->C * h->sum_dim;
+  c.timeout_ticks = (uint64_t)((double)h->opts.consume_timeout_us * h->ticks_per_us);
+  c.so.n_chunks = B / h->C;
+  c.so.per_rank = (B / R) / h->C;
+  c.so.self = h->opts.self_rank;
+  c.so.order = h->opts.chunk_order;
+  c.epoch = expected_epoch;
+  int64_t grid = h->opts.consumer_wgs;
+  if (grid > c.so.n_chunks) grid = c.so.n_chunks;
+  hipError_t e = launch_consume(c, (int)grid, 256, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch consumer kernel");
+  return EBAG_OK;
+}
+
+int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]) {
+  if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
+  HIP_TRY(hipDeviceSynchronize(), "synchronize");
+  int32_t s[4];
+  HIP_TRY(hipMemcpy(s, h->d_status, sizeof s, hipMemcpyDeviceToHost), "read status");
+  out[0] = s[ST_TIMED_OUT];
+  out[1] = s[ST_FIRST_MISSING] == INT_MAX ? -1 : s[ST_FIRST_MISSING];
+  out[2] = s[ST_OVERSHOOT];
+  out[3] = s[ST_FIRST_BAD_BAG] == INT_MAX ? -1 : s[ST_FIRST_BAD_BAG];
+  return EBAG_OK;
+}
+
+int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_flag) {
+  int32_t s[4];
+  int rc = ebag_a2a_status_ex(h, s);
+  if (rc) return rc;
+  if (timed_out) *timed_out = s[0];
+  if (first_missing_flag) *first_missing_flag = s[1];
+  return s[0] ? EBAG_ETIMEOUT : EBAG_OK;
+}
+
+int ebag_a2a_reset(ebag_a2a_t h) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  HIP_TRY(hipDeviceSynchronize(), "synchronize");
+  HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_chunks), "zero counters");
+  HIP_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "reset status");
+  if (h->d_trace_release) {
+    HIP_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+    HIP_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+  }
+  HIP_TRY(hipDeviceSynchronize(), "synchronize");
+  return EBAG_OK;
+}
+
+int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks, int64_t n, double* ticks_per_us) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (!h->d_trace_release) return fail(EBAG_EINVAL, "plan was created without trace = 1");
+  if (n < 0 || n > h->max_chunks) return fail(EBAG_EINVAL, "n=%lld outside [0, %lld]", (long long)n, (long long)h->max_chunks);
+  HIP_TRY(hipDeviceSynchronize(), "synchronize");
+  if (release_ticks && n)
+    HIP_TRY(hipMemcpy(release_ticks, h->d_trace_release, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");
+  if (drain_ticks && n)
+    HIP_TRY(hipMemcpy(drain_ticks, h->d_trace_drain, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");
+  if (ticks_per_us) *ticks_per_us = h->ticks_per_us;
+  return EBAG_OK;
+}
+
+void ebag_a2a_destroy(ebag_a2a_t h) { free_plan(h); }
+
+const char* ebag_a2a_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -106,10 +106,12 @@ class Inputs:
                               VALUE_KIND[self.w.values], self.w.dtype)
 
     def table(self, t: int) -> np.ndarray:
-        """Whole table t materialised on the host (small workloads only)."""
+        """Whole table t materialised on the host."""
         if self.host_tables is not None:
             return self.host_tables[t]
-        return self.table_rows(t, np.arange(self.w.rows[t]))
+        from . import host
+        return host.fill(self.w.rows[t], self.w.dims[t], self.w.dtype, table_seed(self.w.cfg_id, t),
+                         VALUE_KIND[self.w.values])
 
     def unique_rows(self) -> int:
         """Number of distinct (table, row) pairs touched: the DRAM lower bound."""

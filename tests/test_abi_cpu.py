@@ -1,0 +1,95 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad
+arguments before touching the GPU (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ebag_a2a.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ebag_a2a_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2305_06942_amd as ebag
+    return ebag.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    import paper_2305_06942_amd as ebag
+    names = _declared()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in the header but not exported"
+    assert set(names) == set(ebag.symbols()), "binding and header disagree"
+
+
+def test_default_opts(lib):
+    import paper_2305_06942_amd as ebag
+    o = ebag.default_opts()
+    assert (o.waves_per_wg, o.rows_in_flight, o.debug_suppress_flag) == (4, 8, -1)
+
+
+def _create(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, max_batch=256, max_ranks=2, opts=None):
+    import paper_2305_06942_amd.abi as abi
+    h = ctypes.c_void_p()
+    r = (ctypes.c_int64 * len(rows))(*rows)
+    d = (ctypes.c_int32 * len(dims))(*dims)
+    rc = lib.ebag_a2a_create(ctypes.byref(h), T, r, d, dtype, C, max_batch, max_ranks,
+                             None if opts is None else ctypes.byref(opts))
+    return rc, h
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(T=0), "num_tables"),
+    (dict(dims=(64, 6)), "multiple of 16"),
+    (dict(dtype=1, dims=(64, 4)), "multiple of 16"),
+    (dict(dtype=7), "dtype"),
+    (dict(C=0), "chunk_samples"),
+    (dict(max_batch=0), "max_batch"),
+    (dict(rows=(10, -1)), "rows"),
+])
+def test_create_rejects(lib, kw, msg):
+    import paper_2305_06942_amd as ebag
+    rc, h = _create(lib, **kw)
+    assert rc == ebag.abi.EBAG_EINVAL
+    assert msg in ebag.last_error()
+    assert not h.value
+
+
+@pytest.mark.parametrize("field,value,msg", [
+    ("waves_per_wg", 0, "waves_per_wg"), ("waves_per_wg", 17, "waves_per_wg"),
+    ("rows_in_flight", 5, "rows_in_flight"), ("bags_per_run", 0, "bags_per_run"),
+    ("chunk_order", 2, "chunk_order"), ("consumer_wgs", 0, "consumer_wgs"),
+])
+def test_create_rejects_opts(lib, field, value, msg):
+    import paper_2305_06942_amd as ebag
+    o = ebag.default_opts()
+    setattr(o, field, value)
+    rc, _ = _create(lib, opts=o)
+    assert rc == ebag.abi.EBAG_EINVAL and msg in ebag.last_error()
+
+
+def test_null_plan_rejected(lib):
+    import paper_2305_06942_amd as ebag
+    assert lib.ebag_a2a_forward(None, None, None, None, None, 4, 2, None, None, None) == ebag.abi.EBAG_EINVAL
+    assert lib.ebag_a2a_consume(None, None, None, None, 4, 2, 1, None) == ebag.abi.EBAG_EINVAL
+    assert lib.ebag_a2a_reset(None) == ebag.abi.EBAG_EINVAL
+    lib.ebag_a2a_destroy(None)
+
+
+def test_package_has_no_fallback():
+    """The product package never imports the oracle or a CPU path."""
+    pkg = os.path.join(ROOT, "paper_2305_06942_amd")
+    for dp, _, fs in os.walk(pkg):
+        for f in fs:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                src = open(os.path.join(dp, f)).read()
+                assert "oracle" not in src.replace("Oracle", ""), f

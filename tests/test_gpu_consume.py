@@ -1,0 +1,153 @@
+"""Consumer kernel, overlap, and failure paths (timeouts, suppressed flags,
+bad indices) -- every kernel exits normally; failures are forced from the host."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import device as sdev
+from tests.gpu_util import check_full, flags_np, make_plan, new_buffers, run, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+_STREAMS = []
+
+
+def _streams():
+    """Two dedicated streams created back to back (so they sit on different
+    hardware queues); the producer is always enqueued before the consumer, so
+    even if both shared a queue the consumer could only run after it."""
+    import torch
+    if not _STREAMS:
+        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+    return _STREAMS
+
+
+def _concurrent(plan, w, dev, send, recv, flags, epoch, fused=True):
+    import torch
+    main = torch.cuda.current_stream()
+    prod, cons = _streams()
+    prod.wait_stream(main)
+    cons.wait_stream(main)
+    with torch.cuda.stream(prod):
+        run(plan, w, dev, send, flags, fused=fused)
+    with torch.cuda.stream(cons):
+        plan.consume(send, flags, recv, w.B, w.R, epoch)
+    main.wait_stream(prod)
+    main.wait_stream(cons)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_consumer_drains_every_slice(fused):
+    import torch
+    w = synth.TINY
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, trace=1)
+    send, recv, flags = new_buffers(w)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    for epoch in (1, 2, 3):
+        recv.fill_(float("nan"))
+        _concurrent(plan, w, dev, send, recv, flags, epoch, fused)
+        assert plan.status_ex() == (0, -1, 0, -1)
+        assert torch.equal(send.view(torch.int32), recv.view(torch.int32))
+        check_full(inp, recv.cpu().numpy(), s64, a64)
+        assert np.all(flags_np(flags) == epoch)
+        rel, drn, _ = plan.trace(w.n_chunks)
+        assert np.all(rel > 0) and np.all(drn >= rel)
+
+
+@pytest.mark.parametrize("name", ["dlrm", "mixed"])
+def test_overlap_full_size(name):
+    """The consumer drains slices while pooling is still running: the first
+    drain happens before the last slice is released."""
+    import torch
+    w = synth.FULL[name]
+    say("overlap", name)
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, trace=1)
+    send, recv, flags = new_buffers(w)
+    for epoch in (1, 2):
+        _concurrent(plan, w, dev, send, recv, flags, epoch)
+    assert plan.status_ex() == (0, -1, 0, -1)
+    assert torch.equal(send.view(torch.int32), recv.view(torch.int32))
+    assert np.all(flags_np(flags) == 2)
+    rel, drn, tpu = plan.trace(w.n_chunks)
+    assert np.all(drn >= rel)
+    say("overlap", name, "first drain before last release by", (rel.max() - drn.min()) / tpu, "us")
+    assert drn.min() < rel.max()
+
+
+def test_consumer_times_out_without_producer():
+    w = synth.TINY
+    plan = make_plan(w, consume_timeout_us=2000)
+    send, recv, flags = new_buffers(w)
+    plan.consume(send, flags, recv, w.B, w.R, 1)
+    timed_out, missing = plan.status()
+    assert timed_out == 1 and missing == 0
+    plan.reset()
+    assert plan.status_ex() == (0, -1, 0, -1)
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_suppressed_flag_is_named(fused):
+    import torch
+    w = synth.TINY
+    k = 5
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, debug_suppress_flag=k, consume_timeout_us=20000)
+    send, recv, flags = new_buffers(w)
+    _concurrent(plan, w, dev, send, recv, flags, 1, fused)
+    f = flags_np(flags)
+    assert f[k] == 0 and np.all(np.delete(f, k) == 1)
+    timed_out, missing = plan.status()
+    assert timed_out == 1 and missing == k
+    plan.reset()
+    # the data itself is complete even though the flag was withheld
+    check_full(inp, send.cpu().numpy())
+    torch.cuda.synchronize()
+
+
+def test_double_publication_is_reported():
+    """Flags already ahead of the expected epoch are reported, not hidden."""
+    w = synth.TINY
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    send, recv, flags = new_buffers(w)
+    run(plan, w, dev, send, flags)
+    run(plan, w, dev, send, flags)
+    plan.consume(send, flags, recv, w.B, w.R, 1)
+    st = plan.status_ex()
+    assert st[0] == 0 and st[2] == w.n_chunks
+
+
+def test_bad_index_reported_and_skipped():
+    """With check_indices the kernel bounds-checks every index and offset,
+    skips bad rows and names the first bad bag."""
+    import torch
+    w = synth.TINY
+    inp = synth.make_inputs(w)
+    bad_bag = 3 * w.B + 17
+    inp.indices[inp.offsets[bad_bag] + 1] = w.rows[0] + 5
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, check_indices=1)
+    send, _, flags = new_buffers(w)
+    run(plan, w, dev, send, flags)
+    torch.cuda.synchronize()
+    st = plan.status_ex()
+    assert st[3] == bad_bag
+    assert np.all(flags_np(flags) == 1)

@@ -1,0 +1,187 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import device as sdev
+from tests.gpu_util import check_full, check_sampled, flags_np, make_plan, new_buffers, run, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2305_06942_amd as ebag
+    ebag.load()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.F16, synth.BF16])
+@pytest.mark.parametrize("kind", [0, 1])
+def test_device_fill_matches_host(dtype, kind):
+    import torch
+    rows, dim = 1000, 64
+    x = torch.empty((rows, dim), dtype=sdev.torch_dtype(dtype), device="cuda")
+    seed = synth.table_seed(7, 3)
+    sdev.fill_table(x, seed, kind, dtype)
+    torch.cuda.synchronize()
+    got = x.cpu()
+    got = got.view(torch.int16).numpy().view(np.uint16) if dtype != synth.F32 else got.numpy()
+    want = synth.counter_values(seed, dim, np.arange(rows), kind, dtype)
+    assert np.array_equal(got.view(np.uint8), np.ascontiguousarray(want).view(np.uint8))
+
+
+def test_tiny_integer_tables_bit_exact():
+    """Integer-valued tables: exactly one correct fp32 result, in any order."""
+    w = synth.TINY_INT
+    say("tiny_int", w)
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    for fused in (True, False):
+        plan = make_plan(w)
+        send, _, flags = new_buffers(w)
+        for epoch in (1, 2, 3):
+            run(plan, w, dev, send, flags, fused=fused)
+            import torch
+            torch.cuda.synchronize()
+            check_full(inp, send.cpu().numpy(), s64, a64, exact=True)
+            assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, epoch))
+        assert plan.status_ex() == (0, -1, 0, -1)
+
+
+def _small(base):
+    return synth.scaled(base, rows=5000, B=base.R * base.C * 2, T=min(base.T, 12))
+
+
+SMALL = {"tiny": synth.TINY, "dlrm_small": _small(synth.DLRM), "skewed_small": _small(synth.SKEWED),
+         "large_small": _small(synth.LARGE), "mixed_small": _small(synth.MIXED)}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_parity_small_every_element(name):
+    """Every element of fused and unfused results within the tolerance of the
+    oracle, flags bit-exact; both paths produce identical bits."""
+    import torch
+    w = SMALL[name]
+    say("parity", name, w.T, w.B, w.R, w.C)
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    plan = make_plan(w)
+    outs = []
+    for fused in (True, False):
+        send, _, flags = new_buffers(w)
+        run(plan, w, dev, send, flags, fused=fused)
+        torch.cuda.synchronize()
+        got = send.cpu().numpy()
+        check_full(inp, got, s64, a64)
+        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+        outs.append(got)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+
+
+VARIANTS = [
+    dict(waves_per_wg=1), dict(waves_per_wg=16), dict(rows_in_flight=4), dict(rows_in_flight=16),
+    dict(bags_per_run=1), dict(bags_per_run=1000), dict(bags_per_run=5), dict(persistent_wgs_per_cu=2),
+    dict(persistent_wgs_per_cu=-1), dict(release_mode=0), dict(release_mode=0, bags_per_run=64, waves_per_wg=8), dict(chunk_order=1, self_rank=1),
+    dict(check_indices=1),
+]
+
+
+@pytest.mark.parametrize("opts", VARIANTS, ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
+def test_launch_variants(opts):
+    import torch
+    w = SMALL["mixed_small"]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    plan = make_plan(w, **opts)
+    for fused in (True, False):
+        send, _, flags = new_buffers(w)
+        run(plan, w, dev, send, flags, fused=fused)
+        torch.cuda.synchronize()
+        check_full(inp, send.cpu().numpy(), s64, a64)
+        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+    assert plan.status_ex() == (0, -1, 0, -1)
+
+
+def _custom_inputs(dtype, dims, rows, B, R, C, lengths, weighted, seed):
+    rng = np.random.default_rng(seed)
+    w = synth.Workload("custom", 9, len(dims), tuple(rows), tuple(dims), dtype, B, R, C, "fixed:1", "uniform",
+                       weighted, "normal")
+    T = len(dims)
+    L = np.asarray(lengths(rng, T * B), dtype=np.int64)
+    off = np.zeros(T * B + 1, dtype=np.int64)
+    off[1:] = np.cumsum(L)
+    idx = np.concatenate([rng.integers(0, rows[t], size=int(off[(t + 1) * B] - off[t * B]))
+                          for t in range(T)]).astype(np.int32) if off[-1] else np.zeros(0, np.int32)
+    tabs = []
+    for t in range(T):
+        v = rng.standard_normal((rows[t], dims[t])).astype(np.float32)
+        if dtype == synth.F16:
+            v = v.astype(np.float16)
+        elif dtype == synth.BF16:
+            v = synth.gen.f32_to_bf16_bits(v)
+        tabs.append(v)
+    wts = rng.random(int(off[-1]), dtype=np.float32) if weighted else None
+    return synth.Inputs(w, L, off, idx, wts, tabs)
+
+
+EDGE = {
+    "single_sample": (synth.F32, [4], [3], 1, 1, 1, lambda r, n: r.integers(1, 3, n), False),
+    "empty_bags": (synth.F32, [64, 32], [50, 40], 8, 2, 2, lambda r, n: r.integers(0, 2, n) * r.integers(0, 5, n), False),
+    "long_bags_cross_stage": (synth.BF16, [128], [300], 8, 2, 4, lambda r, n: r.integers(120, 400, n), True),
+    "odd_vector_count": (synth.F32, [12, 20, 4], [30, 30, 30], 16, 4, 2, lambda r, n: r.integers(1, 20, n), True),
+    "wide_rows_512": (synth.F32, [512, 1024], [20, 10], 8, 2, 2, lambda r, n: r.integers(1, 40, n), False),
+    "fp16_wide_ragged": (synth.F16, [8, 24, 256, 72], [100, 7, 60, 9], 12, 3, 2, lambda r, n: r.integers(0, 70, n), True),
+    "many_tables": (synth.BF16, [32] * 70, [64] * 70, 4, 2, 1, lambda r, n: r.integers(1, 9, n), False),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_cases(name):
+    import torch
+    inp = _custom_inputs(*EDGE[name], seed=len(name))
+    w = inp.w
+    say("edge", name, w.dims, w.B, w.R, w.C)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    plan = make_plan(w)
+    for fused in (True, False):
+        send, _, flags = new_buffers(w)
+        run(plan, w, dev, send, flags, fused=fused)
+        torch.cuda.synchronize()
+        check_full(inp, send.cpu().numpy(), s64, a64)
+        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+
+
+@pytest.mark.parametrize("name", ["tiny", "dlrm", "skewed", "mixed", "large"])
+def test_full_size_sampled(name):
+    """Full workload sizes: sampled bags element by element against the
+    oracle, every flag equal to the epoch, fused and unfused."""
+    import torch
+    w = synth.FULL[name]
+    say("full", name, "generating inputs")
+    inp = synth.make_inputs(w)
+    say("full", name, "nnz", inp.nnz, "to device")
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    send, _, flags = new_buffers(w)
+    for fused in (True, False):
+        flags.zero_()
+        send.fill_(float("nan"))
+        run(plan, w, dev, send, flags, fused=fused)
+        torch.cuda.synchronize()
+        say("full", name, "fused" if fused else "unfused", "ran; checking")
+        assert not torch.isnan(send).any().item(), "some output element was never written"
+        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+        n = check_sampled(inp, send, n_bags=200)
+        say("full", name, "checked", n, "bags")
+    del dev, send, flags
+    torch.cuda.empty_cache()

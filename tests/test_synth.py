@@ -77,3 +77,25 @@ def test_bf16_rounding_matches_torch():
     ours = gen.f32_to_bf16_bits(x)
     ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
     assert np.array_equal(ours, ref)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.F16, synth.BF16])
+@pytest.mark.parametrize("kind", [0, 1])
+def test_host_fill_matches_numpy(dtype, kind):
+    from synth import host
+    seed = gen.table_seed(4, 9)
+    x = host.fill(777, 24, dtype, seed, kind, nthreads=3)
+    want = gen.counter_values(seed, 24, np.arange(777), kind, dtype)
+    assert np.array_equal(np.ascontiguousarray(x).view(np.uint8), np.ascontiguousarray(want).view(np.uint8))
+
+
+def test_host_half_rounding_matches_numpy():
+    from synth import host
+    lib = host.load()
+    rng = np.random.default_rng(2)
+    xs = np.concatenate([rng.standard_normal(20000).astype(np.float32) * np.float32(0.05),
+                         (rng.standard_normal(20000) * 1e-5).astype(np.float32),
+                         np.array([6.1035156e-05, 6.0975552e-05, 5.96e-08, 2.98e-08, 2.99e-08, 65504.0, 1.0009766,
+                                   1.00048828125, 1.00146484375, -0.0, 0.0], dtype=np.float32)])
+    got = np.array([lib.synth_half_rne(float(v)) for v in xs], dtype=np.uint16)
+    assert np.array_equal(got, xs.astype(np.float16).view(np.uint16))
