@@ -198,6 +198,16 @@ def run_workload(name, steps, warmup, with_cpu, profile):
         "algorithmic_bytes": alg,
     }
     if profile:
+        # a plain copy of known size: calibrates the byte counters per dispatch
+        import torch as _t
+        from synth import device as _sd
+        nb = 1 << 30
+        src = _t.ones(nb // 4, device="cuda")
+        dst = _t.empty_like(src)
+        for _ in range(2):
+            _sd.copy(dst, src, nb)
+        _t.cuda.synchronize()
+        out["calibration_copy_bytes"] = nb
         return out
     # end to end with the concurrent consumer (producer enqueued first)
     prod, cons = torch.cuda.Stream(), torch.cuda.Stream()

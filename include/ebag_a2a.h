@@ -91,7 +91,8 @@ typedef struct ebag_a2a_opts {
   int32_t check_indices;       /* 1: kernels check offsets/indices, skip and report bad bags */
   int32_t debug_suppress_flag; /* >= 0: never publish this slice's flag (failure-path tests); -1 off */
   int32_t consumer_wgs;        /* workgroups of the consumer kernel (default 64) */
-  int32_t reserved;
+  int32_t stream_rows;         /* 1 (default): table rows are read with non-temporal loads (no reuse expected);
+                                  0: cached loads (skewed index distributions with hot rows) */
   int64_t consume_timeout_us;  /* consumer gives up after this long (default 5,000,000 us) */
 } ebag_a2a_opts_t;
 

@@ -30,7 +30,7 @@ class Opts(ctypes.Structure):
         ("check_indices", ctypes.c_int32),
         ("debug_suppress_flag", ctypes.c_int32),
         ("consumer_wgs", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("stream_rows", ctypes.c_int32),
         ("consume_timeout_us", ctypes.c_int64),
     ]
 

@@ -60,7 +60,9 @@ struct PoolArgs {
   int32_t sum_dim;
   int32_t check;              // check offsets / indices
   int32_t release_mode;       // 0 agent-scope release fence, 1 device-scope stores + completion wait
-  int32_t pad;
+  int32_t waves;              // wavefronts per workgroup (blockDim.x / 64)
+  int32_t out_floats;         // LDS output buffer of the fast path: K x max dim
+  int32_t stream_rows;        // 1: table rows loaded non-temporally
 };
 
 struct RepackArgs {
@@ -106,6 +108,7 @@ hipError_t launch_pool(int dtype, int rows_in_flight, bool weighted, bool fused,
 hipError_t launch_repack(const RepackArgs& a, int grid, int block, hipStream_t stream);
 hipError_t launch_publish(const PublishArgs& a, hipStream_t stream);
 hipError_t launch_consume(const ConsumeArgs& a, int grid, int block, hipStream_t stream);
-int pool_max_wgs_per_cu(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, int block);
+int pool_max_wgs_per_cu(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, int block,
+                        int out_floats);
 
 }  // namespace ebag

@@ -1,13 +1,15 @@
 // Host side of the C ABI declared in include/ebag_a2a.h: argument checks,
 // plan-owned device memory, launch geometry and kernel dispatch.
+#include <algorithm>
 #include <climits>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <string>
 #include <vector>
 
-#include "../../include/ebag_a2a.h"
+#include "ebag_a2a.h"
 #include "common.h"
 
 using namespace ebag;
@@ -37,6 +39,63 @@ int hip_fail(hipError_t e, const char* what) {
   } while (0)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Table order inside a slice.  The dispatcher hands workgroups to the XCDs
+// round-robin (workgroup i to XCD i mod n_xcd), and runs are numbered with
+// the table position fastest, so when T is a multiple of n_xcd the runs at
+// positions p, p + n_xcd, ... all land on XCD p mod n_xcd.  Assign tables to
+// XCDs so that every XCD gets T / n_xcd tables with about the same expected
+// bytes (row width; bag lengths are unknown here): widest first, each to the
+// least-loaded XCD with room.  Tables of equal width keep t mod n_xcd, so an
+// XCD's L2 sees the hot rows of only its own tables.  Any order is correct;
+// this only balances work.
+std::vector<int32_t> table_order(const std::vector<int64_t>& row_bytes, int n_xcd) {
+  const int T = (int)row_bytes.size();
+  std::vector<int32_t> perm(T);
+  for (int t = 0; t < T; ++t) perm[t] = t;
+  if (n_xcd <= 1 || T % n_xcd != 0) return perm;
+  std::vector<int32_t> by_width(perm);
+  std::stable_sort(by_width.begin(), by_width.end(),
+                   [&](int32_t x, int32_t y) { return row_bytes[x] > row_bytes[y]; });
+  const int cap = T / n_xcd;
+  std::vector<int64_t> load(n_xcd, 0);
+  std::vector<std::vector<int32_t>> bins(n_xcd);
+  for (int32_t t : by_width) {
+    int best = -1;
+    for (int x = 0; x < n_xcd; ++x)
+      if ((int)bins[x].size() < cap && (best < 0 || load[x] < load[best])) best = x;
+    bins[best].push_back(t);
+    load[best] += row_bytes[t];
+  }
+  // Refine: swap a wider table of the most loaded XCD with a narrower one of
+  // the least loaded while that narrows their gap (each swap strictly lowers
+  // the sum of squared loads, so this ends).
+  for (int it = 0; it < 2 * T; ++it) {
+    const int hi = (int)(std::max_element(load.begin(), load.end()) - load.begin());
+    const int lo = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    const int64_t gap = load[hi] - load[lo];
+    int bi = -1, bj = -1;
+    int64_t bd = 0;
+    for (int i = 0; i < cap; ++i)
+      for (int j = 0; j < cap; ++j) {
+        const int64_t d = row_bytes[bins[hi][i]] - row_bytes[bins[lo][j]];
+        if (d > 0 && d < gap && (bi < 0 || std::llabs(gap - 2 * d) < std::llabs(gap - 2 * bd))) {
+          bi = i;
+          bj = j;
+          bd = d;
+        }
+      }
+    if (bi < 0) break;
+    std::swap(bins[hi][bi], bins[lo][bj]);
+    load[hi] -= bd;
+    load[lo] += bd;
+  }
+  for (int x = 0; x < n_xcd; ++x) {
+    std::sort(bins[x].begin(), bins[x].end());
+    for (int k = 0; k < cap; ++k) perm[x + n_xcd * k] = bins[x][k];
+  }
+  return perm;
+}
 
 int log2_exact(int v) {
   for (int s = 0; s <= 6; ++s)
@@ -99,6 +158,7 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.release_mode < 0 || o.release_mode > 1) return fail(EBAG_EINVAL, "release_mode must be 0 or 1");
   if (o.chunk_order != 0 && o.chunk_order != 1) return fail(EBAG_EINVAL, "chunk_order must be 0 or 1");
   if (o.self_rank < 0) return fail(EBAG_EINVAL, "self_rank must be >= 0");
+  if (o.stream_rows < 0 || o.stream_rows > 1) return fail(EBAG_EINVAL, "stream_rows must be 0 or 1");
   if (o.consumer_wgs < 1) return fail(EBAG_EINVAL, "consumer_wgs must be >= 1");
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   return EBAG_OK;
@@ -148,7 +208,13 @@ int sync_tables(ebag_a2a_plan* h, const void* const* tables, hipStream_t stream)
 void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_t* offsets, const float* weights,
                     int64_t B, const SliceOrder& so, float* out, uint32_t* flags, PoolArgs* a) {
   std::memset(a, 0, sizeof *a);
-  const int32_t K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  int32_t K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  // The fast kernels keep a run's pooled rows in LDS (K x max dim floats):
+  // cap that buffer at 16 KiB.
+  int32_t max_dim = 0;
+  for (const TabMeta& m : h->meta) max_dim = m.dim > max_dim ? m.dim : max_dim;
+  const int32_t k_cap = 16384 / (4 * max_dim) > 1 ? 16384 / (4 * max_dim) : 1;
+  if (K > k_cap) K = k_cap;
   a->tables = h->d_tables;
   a->meta = h->d_meta;
   a->tperm = h->d_tperm;
@@ -171,23 +237,27 @@ void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_
   a->sum_dim = h->sum_dim;
   a->check = h->opts.check_indices;
   a->release_mode = h->opts.release_mode;
+  a->waves = h->opts.waves_per_wg;
+  a->out_floats = K * max_dim;
+  a->stream_rows = h->opts.stream_rows;
 }
 
-// The fast pooling kernels handle row widths of 2^k <= 64 sixteen-byte
-// vectors without index checks; anything else uses the checked kernels.
+// The fast pooling kernels handle tables below 4 GiB (32-bit buffer offsets)
+// whose rows are 2^k <= 64 sixteen-byte vectors, without index reporting;
+// anything else uses the general kernels.
 bool needs_safe(const ebag_a2a_plan* h) {
   if (h->opts.check_indices) return true;
   for (const TabMeta& m : h->meta)
-    if (m.vshift < 0) return true;
+    if (m.vshift < 0 || m.rows * m.row_bytes > (int64_t)0xFFFFFFFFll) return true;
   return false;
 }
 
-int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, int block) {
+int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, int block, int out_floats) {
   int64_t grid = nruns;
   if (h->opts.persistent_wgs_per_cu != 0) {
     int per_cu = h->opts.persistent_wgs_per_cu;
     if (per_cu < 0)
-      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, false, fused, needs_safe(h), block);
+      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, false, fused, needs_safe(h), block, out_floats);
     if (per_cu < 1) per_cu = 1;
     const int64_t pg = (int64_t)per_cu * h->num_cus;
     if (pg < grid) grid = pg;
@@ -214,6 +284,7 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
   o->check_indices = 0;
   o->debug_suppress_flag = -1;
   o->consumer_wgs = 64;
+  o->stream_rows = 1;
   o->consume_timeout_us = 5000000;
   return EBAG_OK;
 }
@@ -287,8 +358,11 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   int khz = 0;
   if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device) == hipSuccess && khz > 0)
     h->ticks_per_us = khz / 1000.0;
-  std::vector<int32_t> tperm(num_tables);
-  for (int32_t t = 0; t < num_tables; ++t) tperm[t] = t;
+  std::vector<int64_t> widths(num_tables);
+  for (int32_t t = 0; t < num_tables; ++t) widths[t] = meta[t].row_bytes;
+  // MI355X: 8 XCDs of 32 CUs.
+  const int n_xcd = (h->num_cus % 32 == 0 && h->num_cus >= 64) ? h->num_cus / 32 : 1;
+  std::vector<int32_t> tperm = table_order(widths, n_xcd);
   CREATE_TRY(hipMalloc((void**)&h->d_meta, sizeof(TabMeta) * num_tables), "alloc table meta");
   CREATE_TRY(hipMemcpy(h->d_meta, meta.data(), sizeof(TabMeta) * num_tables, hipMemcpyHostToDevice), "upload meta");
   CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");
@@ -322,7 +396,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, send_buf, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
-  const int grid = pool_grid(h, a.nruns, true, block);
+  const int grid = pool_grid(h, a.nruns, true, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(h), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
@@ -340,7 +414,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, h->d_scratch, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
-  const int grid = pool_grid(h, a.nruns, false, block);
+  const int grid = pool_grid(h, a.nruns, false, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(h), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch pooling kernel");

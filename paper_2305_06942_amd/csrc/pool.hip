@@ -91,12 +91,36 @@ __device__ __forceinline__ u4v ld_row(const char* colp, int32_t r, uint32_t row_
   return *(gu4v*)(colp + (uint64_t)(uint32_t)r * row_bytes);
 }
 
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
+
+// Row loads through a buffer descriptor covering exactly one table (tables
+// below 4 GiB): 32-bit offsets keep one address register per load instead
+// of two, and the hardware range check turns any offset past the table into
+// zeros, so even invalid indices cannot read outside the table.
+// NT: non-temporal (streaming) loads -- rows that will not be read again do
+// not displace reusable lines (such as the pooled output being written) from
+// L2 and the Infinity Cache.
+template <bool NT>
+struct BufRows {
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t col;  // byte offset of this lane's 16-byte vector inside a row
+  uint32_t rb;   // row bytes
+  __device__ __forceinline__ u4v load(int32_t r) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)r * rb + col, 0, NT ? 2 : 0);
+  }
+};
+
+// Plain 64-bit addressed row loads (any table size).
+struct GlobalRows {
+  const char* colp;
+  uint32_t rb;
+  __device__ __forceinline__ u4v load(int32_t r) const { return ld_row(colp, r, rb); }
+};
+
 // Output stores go through a buffer descriptor spanning exactly one pooled
 // row (out-of-range lanes are dropped by the hardware).  sc1 = 1 gives
 // device-scope stores: they complete at device scope, so a release needs no
 // L2 writeback for them; sc1 = 0 gives plain write-back stores.
-constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
-
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(float* row, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(row, 0, bytes, kBufferWord3);
 }
@@ -115,9 +139,24 @@ __device__ __forceinline__ void store16(__amdgpu_buffer_rsrc_t r, int off, float
 template <bool WT>
 __device__ __forceinline__ void stage(const int32_t* __restrict__ idx, const float* __restrict__ wts, int64_t base,
                                       int n, int lane, int32_t* lds_i, float* lds_w) {
-  for (int i = lane; i < n; i += 64) {
-    lds_i[i] = ((gint*)idx)[base + i];
-    if (WT) lds_w[i] = ((gfloat*)wts)[base + i];
+  // Four 64-index loads in flight before the first LDS write.
+  for (int i0 = 0; i0 < n; i0 += 256) {
+    int32_t x[4];
+    float y[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + 64 * u + lane;
+      x[u] = i < n ? ((gint*)idx)[base + i] : 0;
+      y[u] = (WT && i < n) ? ((gfloat*)wts)[base + i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + 64 * u + lane;
+      if (i < n) {
+        lds_i[i] = x[u];
+        if (WT) lds_w[i] = y[u];
+      }
+    }
   }
 }
 
@@ -127,9 +166,9 @@ __device__ __forceinline__ void stage(const int32_t* __restrict__ idx, const flo
 // branches), then U predicated 16-byte row loads, then the accumulation.
 // Returns true in lanes that met an out-of-range index (CHECK only; such rows
 // are skipped).
-template <class E, int U, bool WT, bool CHECK>
-__device__ __forceinline__ bool gather_p2(const char* colp, uint32_t rb, int vs, int64_t rows,
-                                          const int32_t* li, const float* lw, int n, int lane, float* acc) {
+template <class E, int U, bool WT, bool CHECK, class Rows>
+__device__ __forceinline__ bool gather_p2(const Rows& rows_ld, int vs, int64_t rows, const int32_t* li,
+                                          const float* lw, int n, int lane, float* acc) {
   const int G = 64 >> vs;
   const int g = lane >> vs;
   bool bad = false;
@@ -157,7 +196,7 @@ __device__ __forceinline__ bool gather_p2(const char* colp, uint32_t rb, int vs,
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       raw[u] = u4v{0u, 0u, 0u, 0u};
-      if (ok[u]) raw[u] = ld_row(colp, r[u], rb);
+      if (ok[u]) raw[u] = rows_ld.load(r[u]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) Widen<E>::template add<WT>(acc, raw[u], ok[u] ? wv[u] : 0.f);
@@ -256,6 +295,70 @@ __device__ __forceinline__ void reduce_store(float* acc, int vs, int lane, float
   }
 }
 
+// Values that are the same in every lane but that the compiler cannot prove
+// so (loaded with vector loads from memory the kernel also writes): move them
+// to scalar registers explicitly.
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ int32_t uniform32(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Read-only inputs read with wave-uniform addresses (table order, table
+// constants and pointers, CSR offsets) go through the scalar data cache:
+// their latency then does not queue behind the row gathers in the vector
+// memory pipeline.  Nothing the kernel writes is read this way.
+template <class T>
+__device__ __forceinline__ T sload(const T* p, int64_t i) {
+  return ((const __attribute__((address_space(4))) T*)p)[i];
+}
+
+__device__ __forceinline__ TabMeta load_meta(const TabMeta* p) {
+  TabMeta m;
+  m.rows = sload(&p->rows, 0);
+  m.row_bytes = sload(&p->row_bytes, 0);
+  m.dim = sload(&p->dim, 0);
+  m.col_off = sload(&p->col_off, 0);
+  m.vecs = sload(&p->vecs, 0);
+  m.vshift = sload(&p->vshift, 0);
+  return m;
+}
+
+// Combine the G row groups and write the bag's pooled row (dim floats) into
+// the workgroup's LDS output buffer (lanes of group 0, EPV floats each).
+template <int EPV>
+__device__ __forceinline__ void reduce_to_lds(float* acc, int vs, int lane, float* lrow) {
+  const int V = 1 << vs;
+  for (int msk = 32; msk >= V; msk >>= 1) {
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], msk);
+  }
+  if ((lane >> vs) == 0) {
+    float4* d = reinterpret_cast<float4*>(lrow + (lane & (V - 1)) * EPV);
+#pragma unroll
+    for (int h = 0; h < EPV / 4; ++h) d[h] = make_float4(acc[4 * h], acc[4 * h + 1], acc[4 * h + 2], acc[4 * h + 3]);
+  }
+}
+
+// Write nb pooled rows of dim floats (dim / 4 = 2^s4 float4s each) from LDS
+// to global rows base + i * stride: 64 lanes x 16 bytes per instruction,
+// each row contiguous.
+__device__ __forceinline__ void store_rows(const float* lds, int nb, int s4, float* base, int64_t stride, int dim,
+                                           int lane, bool sc1) {
+  const int n4 = 1 << s4;
+  const int64_t span = ((int64_t)(nb - 1) * stride + dim) * 4;
+  const __amdgpu_buffer_rsrc_t rs = row_rsrc(base, (int)span);
+  const float4* l4 = reinterpret_cast<const float4*>(lds);
+  for (int e = lane; e < (nb << s4); e += 64) {
+    const int i = e >> s4;
+    const int c4 = e & (n4 - 1);
+    const float4 x = l4[e];
+    store16(rs, (int)((int64_t)i * stride * 4) + c4 * 16, x.x, x.y, x.z, x.w, sc1);
+  }
+}
+
 __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
   const int32_t lo = __builtin_amdgcn_readlane((int32_t)(uint32_t)(uint64_t)x, l);
   const int32_t hi = __builtin_amdgcn_readlane((int32_t)((uint64_t)x >> 32), l);
@@ -306,24 +409,32 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
   extern __shared__ int32_t s_dyn[];
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int W = blockDim.x >> 6;
+  const int W = a.waves;
   const int slot = SAFE ? SEG : SEGW;
   int32_t* lds_i = s_dyn + wid * slot;
   float* lds_w = WT ? reinterpret_cast<float*>(s_dyn + W * slot) + wid * slot : nullptr;
+  // Fast path: pooled rows of the current run (K x max dim floats, 16-byte
+  // aligned) and the arrival counter of the run's waves.
+  float* lds_out = reinterpret_cast<float*>(s_dyn + W * slot * (WT ? 2 : 1));
+  int32_t* s_arrive = reinterpret_cast<int32_t*>(lds_out + a.out_floats);
+  if (!SAFE) {
+    if (threadIdx.x == 0) *s_arrive = 0;
+    __syncthreads();
+  }
   const bool sc1 = FUSED && a.release_mode == 1;
   const int64_t per_slice = (int64_t)a.T * a.J;
-  const int64_t nnz = SAFE && a.check ? a.offsets[(int64_t)a.T * a.B] : 0;
+  const int64_t nnz = (!SAFE || a.check) ? sload(a.offsets, (int64_t)a.T * a.B) : 0;
   for (int64_t q = blockIdx.x; q < a.nruns; q += gridDim.x) {
     const int64_t gs = q / per_slice;
     const int64_t rem = q - gs * per_slice;
     const int tpos = (int)(rem % a.T);
     const int j = (int)(rem / a.T);
-    const int t = a.tperm[tpos];
+    const int t = sload(a.tperm, tpos);
     const int64_t g = slice_at(a.so, gs);
     const int64_t b0 = g * a.C + (int64_t)j * a.K;
     const int64_t b1 = min(b0 + (int64_t)a.K, (g + 1) * (int64_t)a.C);
-    const TabMeta m = a.meta[t];
-    const char* tab = static_cast<const char*>(a.tables[t]);
+    const TabMeta m = load_meta(a.meta + t);
+    const char* tab = static_cast<const char*>(sload(a.tables, t));
     const int64_t nb = b1 - b0;
     const int64_t per = (nb + W - 1) / W;
     const int64_t bb = b0 + wid * per;
@@ -332,40 +443,80 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
     const float* outbase = FUSED ? a.out + m.col_off : a.out + a.B * m.col_off;
     const int64_t ostride = FUSED ? a.sum_dim : m.dim;
     if (!SAFE) {
-      const char* colp = tab + (lane & ((1 << m.vshift) - 1)) * 16;
-      const uint32_t rb = (uint32_t)m.row_bytes;
+      BufRows<false> rl;
+      rl.rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(tab), 0, (int)(uint32_t)(m.rows * m.row_bytes),
+                                                kBufferWord3);
+      rl.col = (uint32_t)(lane & ((1 << m.vshift) - 1)) * 16u;
+      rl.rb = (uint32_t)m.row_bytes;
+      BufRows<true> rn;
+      rn.rs = rl.rs;
+      rn.col = rl.col;
+      rn.rb = rl.rb;
+      const bool nt = a.stream_rows;
       for (int64_t blk = bb; blk < be; blk += 63) {
         const int c = (int)min((int64_t)63, be - blk);
-        const int64_t o = lane <= c ? a.offsets[obase + blk + lane] : 0;
-        const int64_t seg_lo = readlane64(o, 0);
-        const int64_t seg_len = readlane64(o, c) - seg_lo;
+        // Offsets are clamped into [0, nnz] and each bag into the block's
+        // segment, so malformed CSR input can never drive a read outside the
+        // index array (results are then meaningless but memory-safe).
+        const int64_t seg_lo = min(max(sload(a.offsets, obase + blk), (int64_t)0), nnz);
+        const int64_t seg_hi = min(max(sload(a.offsets, obase + blk + c), seg_lo), nnz);
+        const int64_t seg_len = seg_hi - seg_lo;
         const bool all = seg_len <= SEGW;
         if (all) {
           stage<WT>(a.indices, a.weights, seg_lo, (int)seg_len, lane, lds_i, lds_w);
           wave_lds_sync();
         }
+        int64_t lo = seg_lo;
         for (int i = 0; i < c; ++i) {
-          const int64_t lo = readlane64(o, i);
-          const int L = (int)(readlane64(o, i + 1) - lo);
+          lo = min(max(sload(a.offsets, obase + blk + i), lo), seg_hi);
+          const int64_t hi = min(max(sload(a.offsets, obase + blk + i + 1), lo), seg_hi);
+          const int L = (int)(hi - lo);
           float acc[EPV];
 #pragma unroll
           for (int e = 0; e < EPV; ++e) acc[e] = 0.f;
           if (all) {
-            gather_p2<E, U, WT, false>(colp, rb, m.vshift, m.rows, lds_i + (lo - seg_lo),
-                                       WT ? lds_w + (lo - seg_lo) : nullptr, L, lane, acc);
+            const int32_t* li = lds_i + (lo - seg_lo);
+            const float* lw = WT ? lds_w + (lo - seg_lo) : nullptr;
+            if (nt)
+              gather_p2<E, U, WT, false>(rn, m.vshift, m.rows, li, lw, L, lane, acc);
+            else
+              gather_p2<E, U, WT, false>(rl, m.vshift, m.rows, li, lw, L, lane, acc);
           } else {
             for (int s0 = 0; s0 < L; s0 += SEGW) {
               const int n = min(SEGW, L - s0);
               stage<WT>(a.indices, a.weights, lo + s0, n, lane, lds_i, lds_w);
               wave_lds_sync();
-              gather_p2<E, U, WT, false>(colp, rb, m.vshift, m.rows, lds_i, lds_w, n, lane, acc);
+              if (nt)
+                gather_p2<E, U, WT, false>(rn, m.vshift, m.rows, lds_i, lds_w, n, lane, acc);
+              else
+                gather_p2<E, U, WT, false>(rl, m.vshift, m.rows, lds_i, lds_w, n, lane, acc);
               wave_lds_sync();
             }
           }
-          reduce_store<EPV>(acc, m.vshift, lane, const_cast<float*>(outbase) + (blk + i) * ostride, m.dim, sc1);
+          reduce_to_lds<EPV>(acc, m.vshift, lane, lds_out + (blk + i - b0) * m.dim);
         }
         if (all) wave_lds_sync();
       }
+      // The last wave to finish its bags writes the whole run from LDS to
+      // global memory and (fused) completes the run for the slice; the other
+      // waves leave at once.  No workgroup barrier on the fast path, and no
+      // store ever sits in front of a gather load of the same wave.
+      int old = 0;
+      if (lane == 0) old = __hip_atomic_fetch_add(s_arrive, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_WORKGROUP);
+      old = __builtin_amdgcn_readfirstlane(old);
+      if (old == W - 1) {
+        if (lane == 0) __hip_atomic_store(s_arrive, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const int s4 = m.vshift + (EPV == 8 ? 1 : 0);
+        store_rows(lds_out, (int)nb, s4, const_cast<float*>(outbase) + b0 * ostride, ostride, m.dim, lane, sc1);
+        if (FUSED) {
+          if (a.release_mode == 1) wait_stores_complete();
+          if (lane == 0)
+            release_slice(a.counters, a.flags, g, (uint32_t)nb, (uint32_t)a.C * (uint32_t)a.T, a.suppress,
+                          a.trace_release, a.release_mode);
+        }
+      }
+      // A persistent workgroup reuses the LDS output buffer for its next run.
+      if (gridDim.x < a.nruns) __syncthreads();
     } else {
       for (int64_t b = bb; b < be; ++b) {
         int64_t lo = a.offsets[obase + b];
@@ -378,7 +529,9 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
         const int L = (int)(hi - lo);
         float* orow = const_cast<float*>(outbase) + b * ostride;
         if (m.vshift >= 0) {
-          const char* colp = tab + (lane & ((1 << m.vshift) - 1)) * 16;
+          GlobalRows rl;
+          rl.colp = tab + (lane & ((1 << m.vshift) - 1)) * 16;
+          rl.rb = (uint32_t)m.row_bytes;
           float acc[EPV];
 #pragma unroll
           for (int e = 0; e < EPV; ++e) acc[e] = 0.f;
@@ -386,10 +539,8 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
             const int n = min(SEG, L - s0);
             stage<WT>(a.indices, a.weights, lo + s0, n, lane, lds_i, lds_w);
             wave_lds_sync();
-            bad |= a.check ? gather_p2<E, U, WT, true>(colp, (uint32_t)m.row_bytes, m.vshift, m.rows, lds_i, lds_w,
-                                                       n, lane, acc)
-                           : gather_p2<E, U, WT, false>(colp, (uint32_t)m.row_bytes, m.vshift, m.rows, lds_i,
-                                                        lds_w, n, lane, acc);
+            bad |= a.check ? gather_p2<E, U, WT, true>(rl, m.vshift, m.rows, lds_i, lds_w, n, lane, acc)
+                           : gather_p2<E, U, WT, false>(rl, m.vshift, m.rows, lds_i, lds_w, n, lane, acc);
             wave_lds_sync();
           }
           reduce_store<EPV>(acc, m.vshift, lane, orow, m.dim, sc1);
@@ -400,7 +551,7 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
         if (a.check && __any(bad) && lane == 0) atomicMin(&a.status[ST_FIRST_BAD_BAG], (int32_t)(obase + b));
       }
     }
-    if (FUSED) {
+    if (FUSED && SAFE) {
       if (a.release_mode == 1) wait_stores_complete();
       __syncthreads();
       if (threadIdx.x == 0)
@@ -453,8 +604,9 @@ pool_fn pick(int dtype, int u, bool weighted, bool fused, bool safe) {
   }
 }
 
-size_t lds_bytes(bool safe, bool weighted, int block) {
-  return (size_t)(block / 64) * (safe ? SEG : SEGW) * (weighted ? 8 : 4);
+size_t lds_bytes(bool safe, bool weighted, int block, int out_floats) {
+  const size_t staging = (size_t)(block / 64) * (safe ? SEG : SEGW) * (weighted ? 8 : 4);
+  return safe ? staging : staging + (size_t)out_floats * 4 + 16;
 }
 
 }  // namespace
@@ -462,14 +614,15 @@ size_t lds_bytes(bool safe, bool weighted, int block) {
 hipError_t launch_pool(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, const PoolArgs& a,
                        int grid, int block, hipStream_t stream) {
   pool_fn f = pick(dtype, rows_in_flight, weighted, fused, safe);
-  hipLaunchKernelGGL(f, dim3(grid), dim3(block), lds_bytes(safe, weighted, block), stream, a);
+  hipLaunchKernelGGL(f, dim3(grid), dim3(block), lds_bytes(safe, weighted, block, a.out_floats), stream, a);
   return hipGetLastError();
 }
 
-int pool_max_wgs_per_cu(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, int block) {
+int pool_max_wgs_per_cu(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, int block,
+                        int out_floats) {
   int n = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, pick(dtype, rows_in_flight, weighted, fused, safe), block,
-                                                   lds_bytes(safe, weighted, block)) != hipSuccess)
+                                                   lds_bytes(safe, weighted, block, out_floats)) != hipSuccess)
     return 0;
   return n;
 }

@@ -90,7 +90,7 @@ VARIANTS = [
     dict(waves_per_wg=1), dict(waves_per_wg=16), dict(rows_in_flight=4), dict(rows_in_flight=16),
     dict(bags_per_run=1), dict(bags_per_run=1000), dict(bags_per_run=5), dict(persistent_wgs_per_cu=2),
     dict(persistent_wgs_per_cu=-1), dict(release_mode=0), dict(release_mode=0, bags_per_run=64, waves_per_wg=8), dict(chunk_order=1, self_rank=1),
-    dict(check_indices=1),
+    dict(check_indices=1), dict(stream_rows=0),
 ]
 
 
