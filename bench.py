@@ -27,6 +27,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public specification
 KERNEL_SOURCES = ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
                   "paper_2305_06942_amd/csrc/repack_consume.hip"]
+# Plan options per workload.  Only the row-cache policy differs: workloads
+# whose indices follow a skewed (Zipf) law re-read hot rows, so their table
+# rows are read through the caches; uniform workloads stream rows (default).
+PLAN_OPTS = {"skewed": {"stream_rows": 0}, "large": {"stream_rows": 0}}
 PAPER_CONTEXT = ("the paper's fused embedding + All-to-All reduced execution time by 20% intra-node "
                  "(4x MI210 over Infinity Fabric, 80 GB/s) and 31% inter-node (2x MI210 over InfiniBand, "
                  "20 GB/s); context only, those numbers include real inter-GPU transport")
@@ -150,7 +154,8 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     dev = sdev.to_device(inp)
     torch.cuda.synchronize()
     alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None)
-    plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R)
+    opts = PLAN_OPTS.get(name, {})
+    plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **opts)
     send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
     recv = torch.empty_like(send)
     flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
@@ -196,6 +201,7 @@ def run_workload(name, steps, warmup, with_cpu, profile):
         "fused_speedup_vs_unfused": round(unfused_ms / fused_ms, 4),
         "pct_hbm_peak": round(100 * alg / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
         "algorithmic_bytes": alg,
+        "plan_options": opts,
     }
     if profile:
         # a plain copy of known size: calibrates the byte counters per dispatch
@@ -210,31 +216,36 @@ def run_workload(name, steps, warmup, with_cpu, profile):
         out["calibration_copy_bytes"] = nb
         return out
     # end to end with the concurrent consumer (producer enqueued first)
-    prod, cons = torch.cuda.Stream(), torch.cuda.Stream()
+    # consumer on a stream with a hardware queue of its own, so it always runs
+    # concurrently with the producer
+    prod, cons = torch.cuda.Stream(), ebag.queue_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev_p, ev_c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e2e = []
-    for it in range(warmup + steps):
-        prod.wait_stream(stream)
-        cons.wait_stream(stream)
-        ev0.record(prod)
-        cons.wait_event(ev0)
-        with torch.cuda.stream(prod):
-            plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
-        epoch[0] += 1
-        with torch.cuda.stream(cons):
-            plan.consume(send, flags, recv, w.B, w.R, epoch[0])
-        ev_p.record(prod)
-        ev_c.record(cons)
-        torch.cuda.synchronize()
-        if it >= warmup:
-            e2e.append(max(ev0.elapsed_time(ev_p), ev0.elapsed_time(ev_c)))
-    st = plan.status_ex()
-    assert st == (0, -1, 0, -1), f"consumer status {st}"
-    assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), "consumer copy differs"
-    out["fused_plus_consumer_us"] = round(1e3 * sorted(e2e)[len(e2e) // 2], 2)
+    for fused_path in (True, False):
+        fwd = plan.forward if fused_path else plan.unfused_forward
+        e2e = []
+        for it in range(warmup + steps):
+            prod.wait_stream(stream)
+            cons.wait_stream(stream)
+            ev0.record(prod)
+            cons.wait_event(ev0)
+            with torch.cuda.stream(prod):
+                fwd(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+            epoch[0] += 1
+            with torch.cuda.stream(cons):
+                plan.consume(send, flags, recv, w.B, w.R, epoch[0])
+            ev_p.record(prod)
+            ev_c.record(cons)
+            torch.cuda.synchronize()
+            if it >= warmup:
+                e2e.append(max(ev0.elapsed_time(ev_p), ev0.elapsed_time(ev_c)))
+        st = plan.status_ex()
+        assert st == (0, -1, 0, -1), f"consumer status {st}"
+        assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), "consumer copy differs"
+        key = "fused_plus_consumer_us" if fused_path else "unfused_plus_consumer_us"
+        out[key] = round(1e3 * sorted(e2e)[len(e2e) // 2], 2)
     # overlap evidence from device timestamps
-    tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1)
+    tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
     prod.wait_stream(stream)
     cons.wait_stream(stream)
     with torch.cuda.stream(prod):
@@ -252,7 +263,8 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     probe, _ = hbm_probe()
     out["hbm_copy_probe_gbs"] = round(probe, 1)
     out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None}
+                       "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None,
+                       "kernel": "fused_pool_kernel"}
     tr = traffic_record(name)
     if tr:
         out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
@@ -295,6 +307,39 @@ def summarize(d):
     return "\n".join(lines)
 
 
+def traffic(fetch_dir, write_dir, workload, kernel="fused_pool_kernel", calib="copy_kernel"):
+    """HBM bytes per launch of `kernel` from two rocprofv3 counter runs of
+    `bench.py --profile` (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch),
+    each scaled by what the same counter reads for the plain copy of
+    calibration_copy_bytes (1 GiB read + 1 GiB written) in the same run."""
+    import csv
+    import statistics
+
+    def per_kernel(d, counter):
+        vals = {}
+        for path in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(path) as f:
+                for r in csv.DictReader(f):
+                    if r["Counter_Name"] == counter:
+                        vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return {k: statistics.median(v) for k, v in vals.items()}
+
+    nb = 1 << 30
+    fe, wr = per_kernel(fetch_dir, "FETCH_SIZE"), per_kernel(write_dir, "WRITE_SIZE")
+    kf = next(k for k in fe if k.startswith(kernel))
+    cf = next(k for k in fe if k.startswith(calib))
+    kw = next(k for k in wr if k.startswith(kernel))
+    cw = next(k for k in wr if k.startswith(calib))
+    f_scale = (nb / 1024.0) / fe[cf]
+    w_scale = (nb / 1024.0) / wr[cw]
+    fetch_b = fe[kf] * f_scale * 1024
+    write_b = wr[kw] * w_scale * 1024
+    return {"workload": workload, "kernel": kernel, "kernel_hash": kernel_hash(),
+            "fetch_kib_raw": fe[kf], "write_kib_raw": wr[kw], "fetch_scale": round(f_scale, 4),
+            "write_scale": round(w_scale, 4), "fetch_bytes": int(fetch_b), "write_bytes": int(write_b),
+            "hbm_bytes_per_launch": int(fetch_b + write_b)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -305,9 +350,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile", action="store_true", help="timing loops only (for rocprofv3 runs)")
     ap.add_argument("--summarize", metavar="DIR")
+    ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
+        return 0
+    if a.traffic:
+        print(json.dumps(traffic(a.traffic[0], a.traffic[1], a.workload), indent=1))
         return 0
     if a.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "

@@ -90,7 +90,7 @@ typedef struct ebag_a2a_opts {
   int32_t trace;               /* 1: record a device timestamp at every slice release and drain */
   int32_t check_indices;       /* 1: kernels check offsets/indices, skip and report bad bags */
   int32_t debug_suppress_flag; /* >= 0: never publish this slice's flag (failure-path tests); -1 off */
-  int32_t consumer_wgs;        /* workgroups of the consumer kernel (default 64) */
+  int32_t consumer_wgs;        /* single-wave workgroups of the consumer kernel (default 512) */
   int32_t stream_rows;         /* 1 (default): table rows are read with non-temporal loads (no reuse expected);
                                   0: cached loads (skewed index distributions with hot rows) */
   int64_t consume_timeout_us;  /* consumer gives up after this long (default 5,000,000 us) */
@@ -142,10 +142,11 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
                              float* send_buf, uint32_t* flags, hipStream_t stream);
 
 /*
- * Receiver side (Sec. III-A, "Book-keeping Flags"): each consumer workgroup
- * owns a distinct subset of slices, polls each slice's flag with acquire
- * semantics until it reaches expected_epoch, then copies the slice from
- * send_buf to recv_buf (same layout and size).  Meant to run on a second
+ * Receiver side (Sec. III-A, "Book-keeping Flags"): each slice is split
+ * into pieces of up to 32 KiB; each consumer workgroup (one wavefront) owns a
+ * distinct subset of pieces, polls the slice's flag until it reaches
+ * expected_epoch, then copies the piece from send_buf to recv_buf (same
+ * layout and size).  Meant to run on a second
  * stream concurrently with a forward.  Enqueue it after the forward it
  * waits for: streams may share a hardware queue, and a consumer queued ahead
  * of its producer on the same queue can only time out.  Polling is bounded
@@ -183,6 +184,15 @@ int ebag_a2a_reset(ebag_a2a_t h);
  */
 int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks, int64_t n,
                    double* ticks_per_us);
+
+/*
+ * Create a HIP stream with a hardware queue of its own (a CU-masked stream
+ * with every CU enabled), for running ebag_a2a_consume concurrently with a
+ * forward: ordinary streams of a process share a few hardware queues, and
+ * two kernels on one queue run one after the other.  Release it with
+ * hipStreamDestroy.
+ */
+int ebag_a2a_queue_stream_create(hipStream_t* out);
 
 /* Release the plan's device memory.  NULL is ignored. */
 void ebag_a2a_destroy(ebag_a2a_t h);

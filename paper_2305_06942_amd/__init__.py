@@ -6,4 +6,4 @@ only: every step of the operation runs in the HIP library
 library is missing, :func:`load` raises.
 """
 from .abi import (EBAG_BF16, EBAG_F16, EBAG_F32, EbagError, Plan, default_opts, last_error,  # noqa: F401
-                  load, symbols)
+                  load, queue_stream, symbols)

@@ -55,6 +55,7 @@ _SIGS = {
     "ebag_a2a_status_ex": ([_P, _P], ctypes.c_int),
     "ebag_a2a_reset": ([_P], ctypes.c_int),
     "ebag_a2a_trace": ([_P, _P, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "ebag_a2a_queue_stream_create": ([_P], ctypes.c_int),
     "ebag_a2a_destroy": ([_P], None),
     "ebag_a2a_last_error": ([], ctypes.c_char_p),
 }
@@ -106,6 +107,14 @@ def _stream(stream) -> Optional[int]:
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
+
+
+def queue_stream():
+    """A torch stream on a hardware queue of its own (ebag_a2a_queue_stream_create)."""
+    import torch
+    s = ctypes.c_void_p()
+    _check(load().ebag_a2a_queue_stream_create(ctypes.byref(s)))
+    return torch.cuda.ExternalStream(s.value)
 
 
 def default_opts() -> Opts:

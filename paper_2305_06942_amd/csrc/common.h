@@ -93,10 +93,12 @@ struct ConsumeArgs {
   int32_t* status;
   uint64_t* trace_drain;
   int64_t chunk_floats;       // C * sum D
+  int64_t piece_f4;           // float4s per work item
+  int64_t pieces;             // work items per slice
   uint64_t timeout_ticks;
   SliceOrder so;
   uint32_t epoch;
-  int32_t pad;
+  int32_t coherent_loads;     // 1: device-scope loads of slice data (no cache invalidation)
 };
 
 // Status word layout (int32[4]).

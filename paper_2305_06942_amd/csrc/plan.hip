@@ -283,7 +283,7 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
   o->trace = 0;
   o->check_indices = 0;
   o->debug_suppress_flag = -1;
-  o->consumer_wgs = 64;
+  o->consumer_wgs = 512;
   o->stream_rows = 1;
   o->consume_timeout_us = 5000000;
   return EBAG_OK;
@@ -466,9 +466,14 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   c.so.self = h->opts.self_rank;
   c.so.order = h->opts.chunk_order;
   c.epoch = expected_epoch;
+  c.coherent_loads = h->opts.release_mode == 1;
+  // Work items of at most 32 KiB per slice.
+  const int64_t chunk_f4 = c.chunk_floats / 4;
+  c.piece_f4 = chunk_f4 < 2048 ? chunk_f4 : 2048;
+  c.pieces = (chunk_f4 + c.piece_f4 - 1) / c.piece_f4;
   int64_t grid = h->opts.consumer_wgs;
-  if (grid > c.so.n_chunks) grid = c.so.n_chunks;
-  hipError_t e = launch_consume(c, (int)grid, 256, stream);
+  if (grid > c.so.n_chunks * c.pieces) grid = c.so.n_chunks * c.pieces;
+  hipError_t e = launch_consume(c, (int)grid, 64, stream);
   if (e != hipSuccess) return hip_fail(e, "launch consumer kernel");
   return EBAG_OK;
 }
@@ -517,6 +522,19 @@ int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks,
   if (drain_ticks && n)
     HIP_TRY(hipMemcpy(drain_ticks, h->d_trace_drain, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");
   if (ticks_per_us) *ticks_per_us = h->ticks_per_us;
+  return EBAG_OK;
+}
+
+int ebag_a2a_queue_stream_create(hipStream_t* out) {
+  if (!out) return fail(EBAG_EINVAL, "null output stream");
+  int dev = 0, cus = 0;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  HIP_TRY(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev), "CU count");
+  // Every CU enabled: the mask only serves to get a hardware queue of the
+  // stream's own.
+  std::vector<uint32_t> mask((cus + 31) / 32, 0u);
+  for (int i = 0; i < cus; ++i) mask[i / 32] |= 1u << (i % 32);
+  HIP_TRY(hipExtStreamCreateWithCUMask(out, (uint32_t)mask.size(), mask.data()), "create stream");
   return EBAG_OK;
 }
 

@@ -38,56 +38,68 @@ __global__ __launch_bounds__(256) void publish_kernel(const PublishArgs a) {
   if (g != a.suppress) __hip_atomic_fetch_add(&a.flags[g], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Receiver: workgroup w owns slices w, w + grid, ... (in production order).
-// For each: one lane polls the flag (relaxed loads, s_sleep back-off,
-// bounded by a wall-clock deadline), then acquires and the whole workgroup
-// copies the slice's C * sum(D) floats from send to recv.
-__global__ __launch_bounds__(256) void consume_kernel(const ConsumeArgs a) {
-  __shared__ int s_state;
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
+
+// Receiver (Sec. III-A, "Book-keeping Flags"): each slice is cut into pieces
+// and the single-wave workgroups take pieces in production order, so the
+// pieces of the slices that complete last are drained by many waves at once.
+// A wave polls the slice flag (relaxed device-scope loads with s_sleep
+// back-off, bounded by a wall-clock deadline), then copies its piece from
+// send to recv.  With coherent_loads the piece is read with device-scope
+// loads, which see the producer's device-scope stores without invalidating
+// this XCD's L2; otherwise an agent-scope acquire precedes plain loads.
+__global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
+  const int lane = threadIdx.x;
   const uint64_t t0 = wall_clock64();
-  const int64_t n4 = a.chunk_floats >> 2;
-  for (int64_t x = blockIdx.x; x < a.so.n_chunks; x += gridDim.x) {
-    const int64_t g = slice_at(a.so, x);
-    if (threadIdx.x == 0) {
-      int st = 0;
-      uint32_t v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      while ((int32_t)(v - a.epoch) < 0) {
-        if (wall_clock64() - t0 > a.timeout_ticks) {
-          st = 1;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(4);
-        v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int64_t n_items = a.so.n_chunks * a.pieces;
+  const int64_t chunk_f4 = a.chunk_floats >> 2;
+  for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
+    const int64_t gs = x / a.pieces;
+    const int64_t p = x - gs * a.pieces;
+    const int64_t g = slice_at(a.so, gs);
+    uint32_t v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    bool timed_out = false;
+    while ((int32_t)(v - a.epoch) < 0) {
+      if (wall_clock64() - t0 > a.timeout_ticks) {
+        timed_out = true;
+        break;
       }
-      if (st == 0) {
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        if (v != a.epoch) st = 2;
-      }
-      s_state = st;
+      __builtin_amdgcn_s_sleep(4);
+      v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __syncthreads();
-    const int st = s_state;
-    if (st == 1) {
-      if (threadIdx.x == 0) {
+    if (__builtin_amdgcn_readfirstlane((int)timed_out)) {
+      if (lane == 0) {
         __hip_atomic_store(&a.status[ST_TIMED_OUT], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         atomicMin(&a.status[ST_FIRST_MISSING], (int32_t)g);
       }
-      return;  // uniform: every thread read the same s_state
+      return;
     }
-    if (st == 2 && threadIdx.x == 0) atomicAdd(&a.status[ST_OVERSHOOT], 1);
-    const float4* src = reinterpret_cast<const float4*>(a.send) + g * n4;
-    float4* dst = reinterpret_cast<float4*>(a.recv) + g * n4;
-    int64_t e = threadIdx.x;
-    for (; e + 3 * (int64_t)blockDim.x < n4; e += 4 * (int64_t)blockDim.x) {
-      const float4 x0 = src[e], x1 = src[e + blockDim.x], x2 = src[e + 2 * blockDim.x], x3 = src[e + 3 * blockDim.x];
-      dst[e] = x0;
-      dst[e + blockDim.x] = x1;
-      dst[e + 2 * blockDim.x] = x2;
-      dst[e + 3 * blockDim.x] = x3;
+    if (v != a.epoch && p == 0 && lane == 0) atomicAdd(&a.status[ST_OVERSHOOT], 1);
+    if (!a.coherent_loads) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const int64_t e0 = p * a.piece_f4;
+    const int n = (int)min(a.piece_f4, chunk_f4 - e0);
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.send + g * a.chunk_floats + e0 * 4), 0, n * 16,
+                                          kBufferWord3);
+    float4* dst = reinterpret_cast<float4*>(a.recv + g * a.chunk_floats) + e0;
+    for (int i0 = 0; i0 < n; i0 += 8 * 64) {
+      u4v r[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * 64 + lane;
+        r[u] = a.coherent_loads ? __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16, 0, 16)
+                                : __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int i = i0 + u * 64 + lane;
+        if (i < n) dst[i] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
+                                        __uint_as_float(r[u].w));
+      }
     }
-    for (; e < n4; e += blockDim.x) dst[e] = src[e];
-    __syncthreads();
-    if (a.trace_drain && threadIdx.x == 0) a.trace_drain[g] = wall_clock64();
+    if (a.trace_drain && lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(&a.trace_drain[g]),
+                                              (unsigned long long)wall_clock64());
   }
 }
 

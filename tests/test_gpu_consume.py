@@ -24,12 +24,12 @@ _STREAMS = []
 
 
 def _streams():
-    """Two dedicated streams created back to back (so they sit on different
-    hardware queues); the producer is always enqueued before the consumer, so
-    even if both shared a queue the consumer could only run after it."""
+    """Producer on an ordinary stream, consumer on a stream with a hardware
+    queue of its own; the producer is enqueued first."""
     import torch
+    import paper_2305_06942_amd as ebag
     if not _STREAMS:
-        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+        _STREAMS.extend([torch.cuda.Stream(), ebag.queue_stream()])
     return _STREAMS
 
 
@@ -88,6 +88,32 @@ def test_overlap_full_size(name):
     assert np.all(drn >= rel)
     say("overlap", name, "first drain before last release by", (rel.max() - drn.min()) / tpu, "us")
     assert drn.min() < rel.max()
+    assert (drn < rel.max()).sum() >= w.n_chunks // 4
+
+
+def test_queue_stream_runs_concurrently():
+    """A consumer enqueued *before* its producer on the dedicated-queue stream
+    still sees every slice: the two kernels run at the same time."""
+    import torch
+    w = synth.FULL["dlrm"]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, consume_timeout_us=2_000_000, trace=1)
+    send, recv, flags = new_buffers(w)
+    main = torch.cuda.current_stream()
+    prod, cons = _streams()
+    prod.wait_stream(main)
+    cons.wait_stream(main)
+    for epoch in (1, 2, 3):
+        with torch.cuda.stream(cons):
+            plan.consume(send, flags, recv, w.B, w.R, epoch)
+        with torch.cuda.stream(prod):
+            run(plan, w, dev, send, flags)
+        torch.cuda.synchronize()
+        assert plan.status_ex() == (0, -1, 0, -1), f"epoch {epoch}"
+        rel, drn, tpu = plan.trace(w.n_chunks)
+        assert drn.min() < rel.max(), "no slice was drained while pooling was still running"
+    assert torch.equal(send.view(torch.int32), recv.view(torch.int32))
 
 
 def test_consumer_times_out_without_producer():
