@@ -99,7 +99,7 @@ def hbm_probe(nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9, ms
 
 
-def cpu_baseline(w, inp, bytes_fn, max_tables=None):
+def cpu_baseline(w, inp, bytes_fn, max_tables=None, min_seconds=10.0):
     """The CPU oracle timed on this host's cores over the first tables of the
     same workload (all B samples of each)."""
     import numpy as np
@@ -121,13 +121,15 @@ def cpu_baseline(w, inp, bytes_fn, max_tables=None):
     wts = None if inp.weights is None else inp.weights[:int(off[-1])]
     sub = w.with_(T=T, rows=w.rows[:T], dims=w.dims[:T])
     nbytes = bytes_fn(sub, inp.lengths[:T * w.B], inp.weights is not None)
+    # Repeat the pass until about min_seconds of CPU time have been measured
+    # (at least 3 passes) and report the median pass.
     times = []
-    for _ in range(3):
+    while len(times) < 3 or sum(times) < min_seconds:
         t0 = time.time()
         oracle.pool(tables, w.dtype, sub.dims, idx, off, wts, w.B, w.R, w.C, nthreads=cores,
                     want_abs=False, want_sum=True, want_send=True)
         times.append(time.time() - t0)
-    med = sorted(times)[1]
+    med = sorted(times)[len(times) // 2]
     cpu_model = ""
     try:
         cpu_model = [l.split(":", 1)[1].strip() for l in open("/proc/cpuinfo") if l.startswith("model name")][0]
@@ -135,8 +137,41 @@ def cpu_baseline(w, inp, bytes_fn, max_tables=None):
         pass
     return {"value": round(nbytes / med / 1e9, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
             "sample": f"C oracle (fp64) over tables 0..{T - 1} of {w.T}, all {w.B} samples "
-                      f"({nbytes / 1e9:.2f} GB algorithmic), median of 3 runs, {med:.3f} s each; "
+                      f"({nbytes / 1e9:.2f} GB algorithmic), median of {len(times)} passes ({sum(times):.1f} s in all), "
+                      f"{med:.3f} s per pass; "
                       f"host tables generated in {gen_s:.1f} s (not timed); CPU {cpu_model}"}
+
+
+def e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, consumer_first, prod, cons, stream, steps, warmup):
+    """Median microseconds from the start of the first enqueued kernel to the
+    end of both the forward (on prod) and the consumer (on cons).  epoch is a
+    one-element list holding the flags' current epoch."""
+    import torch
+    fwd = plan.forward if fused_path else plan.unfused_forward
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev_p, ev_c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    first, second = (cons, prod) if consumer_first else (prod, cons)
+    times = []
+    for it in range(warmup + steps):
+        first.wait_stream(stream)
+        ev0.record(first)
+        second.wait_event(ev0)
+        epoch[0] += 1
+        for s in (first, second):
+            with torch.cuda.stream(s):
+                if s is prod:
+                    fwd(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+                else:
+                    plan.consume(send, flags, recv, w.B, w.R, epoch[0])
+        ev_p.record(prod)
+        ev_c.record(cons)
+        torch.cuda.synchronize()
+        if it >= warmup:
+            times.append(max(ev0.elapsed_time(ev_p), ev0.elapsed_time(ev_c)))
+    st = plan.status_ex()
+    assert st == (0, -1, 0, -1), f"consumer status {st}"
+    assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), "consumer copy differs"
+    return round(1e3 * sorted(times)[len(times) // 2], 2) if times else None
 
 
 def run_workload(name, steps, warmup, with_cpu, profile):
@@ -215,48 +250,20 @@ def run_workload(name, steps, warmup, with_cpu, profile):
         _t.cuda.synchronize()
         out["calibration_copy_bytes"] = nb
         return out
-    # end to end with the concurrent consumer (producer enqueued first)
-    # consumer on a stream with a hardware queue of its own, so it always runs
-    # concurrently with the producer
-    prod, cons = torch.cuda.Stream(), ebag.queue_stream()
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev_p, ev_c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # End to end with the concurrent consumer: producer enqueued first, each
+    # on a stream with a hardware queue of its own, so the two always run
+    # concurrently.
+    prod, cons = ebag.queue_stream(), ebag.queue_stream()
     for fused_path in (True, False):
-        fwd = plan.forward if fused_path else plan.unfused_forward
-        e2e = []
-        for it in range(warmup + steps):
-            prod.wait_stream(stream)
-            cons.wait_stream(stream)
-            ev0.record(prod)
-            cons.wait_event(ev0)
-            with torch.cuda.stream(prod):
-                fwd(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
-            epoch[0] += 1
-            with torch.cuda.stream(cons):
-                plan.consume(send, flags, recv, w.B, w.R, epoch[0])
-            ev_p.record(prod)
-            ev_c.record(cons)
-            torch.cuda.synchronize()
-            if it >= warmup:
-                e2e.append(max(ev0.elapsed_time(ev_p), ev0.elapsed_time(ev_c)))
-        st = plan.status_ex()
-        assert st == (0, -1, 0, -1), f"consumer status {st}"
-        assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), "consumer copy differs"
-        key = "fused_plus_consumer_us" if fused_path else "unfused_plus_consumer_us"
-        out[key] = round(1e3 * sorted(e2e)[len(e2e) // 2], 2)
+        key = ("fused" if fused_path else "unfused") + "_plus_consumer_us"
+        out[key] = e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, False, prod, cons, stream, steps, warmup)
     # overlap evidence from device timestamps
     tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
-    prod.wait_stream(stream)
-    cons.wait_stream(stream)
-    with torch.cuda.stream(prod):
-        tplan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
-    epoch[0] += 1
-    with torch.cuda.stream(cons):
-        tplan.consume(send, flags, recv, w.B, w.R, epoch[0])
-    torch.cuda.synchronize()
+    e2e_us(tplan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, 0)
     rel, drn, tpu = tplan.trace(w.n_chunks)
     out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
     out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
+    out["median_drain_lag_us"] = round(float(np.median(drn.astype(np.int64) - rel.astype(np.int64))) / tpu, 2)
     out["n_slices"] = w.n_chunks
     rows_alg = int(sum(int(inp.lengths.reshape(w.T, w.B)[t].sum()) * w.dims[t] * w.elt for t in range(w.T)))
     out["unique_row_gbs"] = round((alg - rows_alg + inp.unique_row_bytes()) / (fused_ms * 1e-3) / 1e9, 2)
@@ -274,6 +281,91 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     if with_cpu:
         log(f"[{name}] timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes)
+    return out
+
+
+def _setup(name):
+    import torch
+    import synth
+    from synth import device as sdev
+    w = synth.FULL[name]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
+    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    return w, inp, dev, send, flags
+
+
+def run_occupancy(name, steps, warmup):
+    """Fused-kernel time versus the fraction of resident workgroup slots a
+    persistent grid occupies (Sec. IV-C, Fig. 13), for 2, 4 and 8 waves per
+    workgroup, next to the default one-workgroup-per-run grid."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    w, inp, dev, send, flags = _setup(name)
+    alg = algorithmic_bytes(w, inp.lengths, w.weighted)
+    base = dict(PLAN_OPTS.get(name, {}))
+    s = torch.cuda.current_stream()
+    rows = []
+    for waves in (2, 4, 8):
+        probe = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, waves_per_wg=waves, **base)
+        max_wgs, cus, block, K = probe.occupancy(w.weighted)
+        probe.close()
+        for per_cu in [0] + list(range(1, max_wgs + 1)):
+            plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, waves_per_wg=waves,
+                             persistent_wgs_per_cu=per_cu, **base)
+            f = lambda: plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, send, flags)
+            for _ in range(warmup):
+                f()
+            ms = time_launches(f, steps, s)
+            plan.close()
+            row = {"workload": name, "waves_per_wg": waves, "persistent_wgs_per_cu": per_cu,
+                   "max_wgs_per_cu": max_wgs, "occupancy": round(per_cu / max_wgs, 4) if per_cu else None,
+                   "grid": "one workgroup per run" if per_cu == 0 else f"{per_cu * cus} persistent",
+                   "fused_us": round(ms * 1e3, 2), "gbs": round(alg / (ms * 1e-3) / 1e9, 1)}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+    return rows
+
+
+def run_timeline(name, warmup):
+    """Per-slice release and drain times of one traced forward + concurrent
+    consumer (enqueued after it, on its own hardware queue), in natural slice order and in communication-aware order
+    (destination self_rank = 0 kept local and produced last; Sec. III-A,
+    Sec. IV-C, Fig. 14).  Times in us from the first release."""
+    import numpy as np
+    import torch
+    import paper_2305_06942_amd as ebag
+    w, inp, dev, send, flags = _setup(name)
+    recv = torch.empty_like(send)
+    base = dict(PLAN_OPTS.get(name, {}))
+    prod, cons = ebag.queue_stream(), ebag.queue_stream()
+    stream = torch.cuda.current_stream()
+    epoch = [0]
+    per = w.n_chunks // w.R
+    out = []
+    for order in (0, 1):
+        plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, chunk_order=order, self_rank=0, **base)
+        e2e_us(plan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, warmup)
+        assert plan.status_ex() == (0, -1, 0, -1)
+        rel, drn, tpu = plan.trace(w.n_chunks)
+        t0 = int(rel.min())
+        r_us = (rel.astype(np.int64) - t0) / tpu
+        d_us = (drn.astype(np.int64) - t0) / tpu
+        remote = np.ones(w.n_chunks, dtype=bool)
+        remote[0:per] = False  # destination 0 is the local one
+        row = {"workload": name, "chunk_order": order, "self_rank": 0, "n_slices": w.n_chunks,
+               "last_release_us": round(float(r_us.max()), 2),
+               "last_remote_release_us": round(float(r_us[remote].max()), 2),
+               "last_local_release_us": round(float(r_us[~remote].max()), 2),
+               "last_remote_drain_us": round(float(d_us[remote].max()), 2),
+               "last_drain_us": round(float(d_us.max()), 2),
+               "median_drain_lag_us": round(float(np.median(d_us - r_us)), 2),
+               "release_us_by_slice": [round(float(x), 1) for x in r_us],
+               "drain_us_by_slice": [round(float(x), 1) for x in d_us]}
+        plan.close()
+        out.append(row)
+        print(json.dumps(row), flush=True)
     return out
 
 
@@ -351,6 +443,8 @@ def main():
     ap.add_argument("--profile", action="store_true", help="timing loops only (for rocprofv3 runs)")
     ap.add_argument("--summarize", metavar="DIR")
     ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--occupancy", action="store_true", help="persistent-grid occupancy sweep of the fused kernel")
+    ap.add_argument("--timeline", action="store_true", help="per-slice release / drain times, both slice orders")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -367,6 +461,12 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
     torch.cuda.set_device(0)
+    if a.occupancy:
+        run_occupancy(a.workload, a.steps, a.warmup)
+        return 0
+    if a.timeline:
+        run_timeline(a.workload, a.warmup)
+        return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:
         out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile)

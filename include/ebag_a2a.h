@@ -186,6 +186,17 @@ int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks,
                    double* ticks_per_us);
 
 /*
+ * Launch geometry of this plan's fused pooling kernel, for sizing persistent
+ * grids (the occupancy study of Sec. IV-C: time versus the fraction of
+ * resident workgroup slots in use, Fig. 13).  weighted selects the weighted-sum
+ * kernel.  out[0]: workgroups of that kernel that fit on one CU at once
+ * (registers and LDS, from the HIP occupancy query); out[1]: CUs of the
+ * plan's device; out[2]: threads per workgroup; out[3]: bags per run (K).
+ * Returns EBAG_OK, EBAG_EINVAL (null argument) or EBAG_EHIP.
+ */
+int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]);
+
+/*
  * Create a HIP stream with a hardware queue of its own (a CU-masked stream
  * with every CU enabled), for running ebag_a2a_consume concurrently with a
  * forward: ordinary streams of a process share a few hardware queues, and

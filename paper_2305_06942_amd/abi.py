@@ -55,6 +55,7 @@ _SIGS = {
     "ebag_a2a_status_ex": ([_P, _P], ctypes.c_int),
     "ebag_a2a_reset": ([_P], ctypes.c_int),
     "ebag_a2a_trace": ([_P, _P, _P, ctypes.c_int64, _P], ctypes.c_int),
+    "ebag_a2a_occupancy": ([_P, ctypes.c_int32, _P], ctypes.c_int),
     "ebag_a2a_queue_stream_create": ([_P], ctypes.c_int),
     "ebag_a2a_destroy": ([_P], None),
     "ebag_a2a_last_error": ([], ctypes.c_char_p),
@@ -189,6 +190,12 @@ class Plan:
         tpu = ctypes.c_double()
         _check(self._lib.ebag_a2a_trace(self._h, rel.ctypes.data, drn.ctypes.data, n, ctypes.byref(tpu)))
         return rel, drn, tpu.value
+
+    def occupancy(self, weighted=False):
+        """(max resident WGs per CU, CUs, threads per WG, bags per run) of the fused kernel."""
+        s = (ctypes.c_int32 * 4)()
+        _check(self._lib.ebag_a2a_occupancy(self._h, int(bool(weighted)), s))
+        return tuple(s)
 
     def close(self):
         if getattr(self, "_h", None):

@@ -252,12 +252,13 @@ bool needs_safe(const ebag_a2a_plan* h) {
   return false;
 }
 
-int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, int block, int out_floats) {
+int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, bool weighted, int block, int out_floats) {
   int64_t grid = nruns;
   if (h->opts.persistent_wgs_per_cu != 0) {
     int per_cu = h->opts.persistent_wgs_per_cu;
     if (per_cu < 0)
-      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, false, fused, needs_safe(h), block, out_floats);
+      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, weighted, fused, needs_safe(h), block,
+                                   out_floats);
     if (per_cu < 1) per_cu = 1;
     const int64_t pg = (int64_t)per_cu * h->num_cus;
     if (pg < grid) grid = pg;
@@ -396,7 +397,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, send_buf, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
-  const int grid = pool_grid(h, a.nruns, true, block, a.out_floats);
+  const int grid = pool_grid(h, a.nruns, true, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(h), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
@@ -414,7 +415,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, h->d_scratch, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
-  const int grid = pool_grid(h, a.nruns, false, block, a.out_floats);
+  const int grid = pool_grid(h, a.nruns, false, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(h), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch pooling kernel");
@@ -522,6 +523,26 @@ int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks,
   if (drain_ticks && n)
     HIP_TRY(hipMemcpy(drain_ticks, h->d_trace_drain, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");
   if (ticks_per_us) *ticks_per_us = h->ticks_per_us;
+  return EBAG_OK;
+}
+
+int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]) {
+  if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
+  HIP_TRY(hipSetDevice(h->device), "set device");
+  // Same launch shape as a forward: the LDS tile does not depend on B.
+  PoolArgs a;
+  SliceOrder so;
+  std::memset(&so, 0, sizeof so);
+  fill_pool_args(h, nullptr, nullptr, nullptr, 0, so, nullptr, nullptr, &a);
+  const int block = 64 * h->opts.waves_per_wg;
+  const int n = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, weighted != 0, true, needs_safe(h), block,
+                                    a.out_floats);
+  if (n <= 0) return fail(EBAG_EHIP, "occupancy query failed");
+  out[0] = n;
+  out[1] = h->num_cus;
+  out[2] = block;
+  out[3] = a.K;
+  g_err.clear();
   return EBAG_OK;
 }
 

@@ -185,3 +185,26 @@ def test_full_size_sampled(name):
         say("full", name, "checked", n, "bags")
     del dev, send, flags
     torch.cuda.empty_cache()
+
+
+def test_occupancy_query_and_full_persistent_grid():
+    """ebag_a2a_occupancy reports the launch shape; a persistent grid of
+    exactly that many workgroups per CU (weighted kernel) gives the same
+    result as the one-workgroup-per-run grid."""
+    import torch
+    w = SMALL["mixed_small"]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    for waves in (2, 4):
+        probe = make_plan(w, waves_per_wg=waves)
+        max_wgs, cus, block, K = probe.occupancy(True)
+        probe.close()
+        assert cus == torch.cuda.get_device_properties(0).multi_processor_count
+        assert block == 64 * waves and 1 <= K <= w.C and max_wgs >= 1
+        plan = make_plan(w, waves_per_wg=waves, persistent_wgs_per_cu=max_wgs)
+        send, _, flags = new_buffers(w)
+        run(plan, w, dev, send, flags, fused=True)
+        torch.cuda.synchronize()
+        check_full(inp, send.cpu().numpy(), s64, a64)
+        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
