@@ -49,7 +49,7 @@ def load(path: str = LIB):
     lib = ctypes.CDLL(path)
     P = ctypes.c_void_p
     i32, i64 = ctypes.c_int32, ctypes.c_int64
-    lib.oracle_pool.argtypes = [i32, P, P, P, i32, P, i64, P, P, i64, i32, i32, P, P, P, i32]
+    lib.oracle_pool.argtypes = [i32, P, P, P, i32, P, i64, P, P, i32, i64, i32, i32, P, P, P, i32]
     lib.oracle_pool.restype = ctypes.c_int
     lib.oracle_validate.argtypes = [i32, P, P, P, i64, P, i64, i32, i32]
     lib.oracle_validate.restype = ctypes.c_int
@@ -73,9 +73,10 @@ def _ptr(a):
 
 
 def pool(tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=None, lib=None,
-         want_sum=True, want_abs=True, want_send=True):
+         want_sum=True, want_abs=True, want_send=True, mean=False):
     """Pool one forward.  ``tables`` is a list of host arrays in storage dtype
     (float32, float16, or uint16 bf16 bits), shape (rows_t, dims[t]).
+    ``mean``: mean pooling (sum / L, zeros for empty bags; no weights).
 
     Returns (sum64, abs64, send) with shape (B, sum(D)) each; ``send`` is the
     fp32 send buffer, whose memory order is [R][B/R][sum(D)].
@@ -97,7 +98,7 @@ def pool(tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=None,
         nthreads = len(os.sched_getaffinity(0))
     rc = lib.oracle_pool(T, ctypes.cast(ptrs, ctypes.c_void_p), rows.ctypes.data, dims.ctypes.data, dtype,
                          _ptr(indices) if indices.size else None, indices.size, offsets.ctypes.data,
-                         _ptr(weights), B, R, C, _ptr(sum64), _ptr(abs64), _ptr(send), nthreads)
+                         _ptr(weights), int(bool(mean)), B, R, C, _ptr(sum64), _ptr(abs64), _ptr(send), nthreads)
     if rc != 0:
         raise OracleError(f"oracle_pool: {ERRORS.get(rc, rc)}")
     return sum64, abs64, send

@@ -12,9 +12,10 @@ per (destination, slice of C samples), equal to the number of forwards.
 from __future__ import annotations
 
 
-def pool(tables, indices, offsets, weights, B, R):
+def pool(tables, indices, offsets, weights, B, R, mean=False):
     """tables: list of T lists of rows (each row a list of numbers).
-    Returns send as a nested list send[r][s][col] of Python floats."""
+    Returns send as a nested list send[r][s][col] of Python floats; mean=True
+    divides each bag's sum by its length (an empty bag stays zero)."""
     T = len(tables)
     dims = [len(tab[0]) for tab in tables]
     S = B // R
@@ -30,6 +31,8 @@ def pool(tables, indices, offsets, weights, B, R):
                 for k in range(lo, hi):
                     w = 1.0 if weights is None else float(weights[k])
                     acc += w * float(tables[t][indices[k]][j])
+                if mean and hi > lo:
+                    acc /= hi - lo
                 send[r][s][col + j] = acc
         col += dims[t]
     return send

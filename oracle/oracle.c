@@ -8,10 +8,13 @@
  * What it computes (the plain definition the fused operator must reach):
  *
  *   Embedding pooling (Sec. III-A): one logical workgroup of the original
- *   EmbeddingBag kernel produces one pooled output vector; for table t and
- *   sample b the bag is the index run offsets[t*B+b] .. offsets[t*B+b+1] and
- *   the output is the (optionally per-index weighted) sum of the indexed rows.
- *   Accumulation is in fp64, in index order; fp32/fp16/bf16 widen exactly.
+ *   EmbeddingBag kernel (a sum / mean pooling kernel) produces one pooled
+ *   output vector; for table t and sample b the bag is the index run
+ *   offsets[t*B+b] .. offsets[t*B+b+1] and the output is the (optionally
+ *   per-index weighted) sum of the indexed rows, or in mean mode that sum
+ *   divided by the bag length L (zeros for an empty bag; mean takes no
+ *   weights).  Accumulation is in fp64, in index order; fp32/fp16/bf16 widen
+ *   exactly.
  *
  *   All-to-All placement (Sec. III-A, worked example): the global batch is
  *   split into R equal contiguous parts, the first part going to destination
@@ -106,6 +109,7 @@ typedef struct {
   const int32_t* indices;
   const int64_t* offsets;
   const float* weights;
+  int32_t mean;
   int64_t B;
   int32_t R;
   double* sum64;
@@ -135,6 +139,10 @@ static void* pool_range(void* arg) {
           sum += term;
           mag += fabs(term);
         }
+        if (J->mean && hi > lo) {
+          sum /= (double)(hi - lo);
+          mag /= (double)(hi - lo);
+        }
         if (J->sum64) J->sum64[out + j] = sum;
         if (J->abs64) J->abs64[out + j] = mag;
         if (J->send) J->send[out + j] = (float)sum;
@@ -149,14 +157,16 @@ static void* pool_range(void* arg) {
  *   tables   : T host pointers, table t is rows[t] x dims[t], row-major, dtype
  *   indices  : int32 [nnz], table-major CSR; offsets: int64 [T*B + 1]
  *   weights  : fp32 [nnz] or NULL (plain sum)
+ *   mode     : 0 sum, 1 mean (weights must then be NULL)
  *   sum64/abs64 : [B * sum(D)] fp64 (either may be NULL); send: fp32 [B * sum(D)]
  *   nthreads : worker threads over sample ranges (<= 0 means 1)
  * Returns OR_OK or a negative OR_* code (outputs untouched on error).
  */
 int oracle_pool(int32_t T, const void* const* tables, const int64_t* rows, const int32_t* dims, int32_t dtype,
-                const int32_t* indices, int64_t nnz, const int64_t* offsets, const float* weights, int64_t B,
-                int32_t R, int32_t C, double* sum64, double* abs64, float* send, int32_t nthreads) {
+                const int32_t* indices, int64_t nnz, const int64_t* offsets, const float* weights, int32_t mode,
+                int64_t B, int32_t R, int32_t C, double* sum64, double* abs64, float* send, int32_t nthreads) {
   if (!tables || dtype < OR_F32 || dtype > OR_BF16) return OR_BAD_ARGS;
+  if (mode < 0 || mode > 1 || (mode == 1 && weights)) return OR_BAD_ARGS;
   int rc = oracle_validate(T, rows, dims, indices, nnz, offsets, B, R, C);
   if (rc != OR_OK) return rc;
   int64_t* col_off = (int64_t*)malloc(sizeof(int64_t) * (size_t)T);
@@ -171,8 +181,8 @@ int oracle_pool(int32_t T, const void* const* tables, const int64_t* rows, const
   job_t* jobs = (job_t*)calloc((size_t)nthreads, sizeof(job_t));
   pthread_t* th = (pthread_t*)calloc((size_t)nthreads, sizeof(pthread_t));
   for (int32_t i = 0; i < nthreads; ++i) {
-    job_t J = {T, tables, dims, col_off, sum_dim, dtype, indices, offsets, weights, B, R, sum64, abs64, send,
-               B * i / nthreads, B * (i + 1) / nthreads};
+    job_t J = {T, tables, dims, col_off, sum_dim, dtype, indices, offsets, weights, mode, B, R, sum64, abs64,
+               send, B * i / nthreads, B * (i + 1) / nthreads};
     jobs[i] = J;
   }
   for (int32_t i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, pool_range, &jobs[i]);

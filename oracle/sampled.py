@@ -44,8 +44,9 @@ def flat_row(B, R, b):
     return r * S + s
 
 
-def pool_bag(inputs, t, b):
-    """fp64 (sum, sum of |terms|) of bag (t, b), each of length D_t."""
+def pool_bag(inputs, t, b, mean=False):
+    """fp64 (sum, sum of |terms|) of bag (t, b), each of length D_t; with
+    mean=True both divided by the bag length (zeros for an empty bag)."""
     w = inputs.w
     lo, hi = int(inputs.offsets[t * w.B + b]), int(inputs.offsets[t * w.B + b + 1])
     D = w.dims[t]
@@ -59,10 +60,13 @@ def pool_bag(inputs, t, b):
     for k in range(rows.shape[0]):      # index order, like the definition
         s += rows[k]
         a += np.abs(rows[k])
+    if mean:
+        s /= rows.shape[0]
+        a /= rows.shape[0]
     return s, a
 
 
-def pool_bags(inputs, bags):
+def pool_bags(inputs, bags, mean=False):
     """Expected values for a list of (t, b) bags.
 
     Returns a list of (t, b, flat_row, col0, sum64, abs64)."""
@@ -70,7 +74,7 @@ def pool_bags(inputs, bags):
     off = column_offsets(w.dims)
     out = []
     for t, b in bags:
-        s, a = pool_bag(inputs, int(t), int(b))
+        s, a = pool_bag(inputs, int(t), int(b), mean)
         out.append((int(t), int(b), flat_row(w.B, w.R, int(b)), int(off[t]), s, a))
     return out
 

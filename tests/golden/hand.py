@@ -1,4 +1,5 @@
 """Parser for the hand-worked fixture ``hand_example.txt``."""
+import fractions
 import os
 
 import numpy as np
@@ -7,7 +8,7 @@ PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "hand_example.tx
 
 
 def load(path=PATH):
-    d = {"tables": [], "sum": {}, "wsum": {}}
+    d = {"tables": [], "sum": {}, "wsum": {}, "mean": {}}
     cur = None
     with open(path) as f:
         for line in f:
@@ -27,15 +28,16 @@ def load(path=PATH):
             elif key == "weights":
                 d[key] = [float(x) for x in rest]
                 cur = None
-            elif key in ("sum", "wsum"):
+            elif key in ("sum", "wsum", "mean"):
                 r, s, *vals = rest
-                d[key][(int(r), int(s))] = [float(x) for x in vals]
+                # exact rationals, rounded once to the nearest double
+                d[key][(int(r), int(s))] = [float(fractions.Fraction(x)) for x in vals]
                 cur = None
             else:
                 cur.append([float(x) for x in [key] + rest])
     R, B = d["R"], d["B"]
     S = B // R
-    for k in ("sum", "wsum"):
+    for k in ("sum", "wsum", "mean"):
         arr = np.zeros((R, S, len(next(iter(d[k].values())))))
         for (r, s), v in d[k].items():
             arr[r, s] = v

@@ -23,8 +23,9 @@ import oracle
 from tests.golden import hand
 
 
-def _pool(lib, tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=2):
-    return oracle.pool(tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=nthreads, lib=lib)
+def _pool(lib, tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=2, mean=False):
+    return oracle.pool(tables, dtype, dims, indices, offsets, weights, B, R, C, nthreads=nthreads, lib=lib,
+                       mean=mean)
 
 
 def pin_hand(lib):
@@ -42,6 +43,9 @@ def pin_hand(lib):
     s64, a64, send = _pool(lib, tabs, 0, dims, idx, off, w, B, R, C)
     assert np.array_equal(s64.reshape(R, S, -1), d["wsum"]), "hand weighted sum"
     assert np.array_equal(send.reshape(R, S, -1), d["wsum"].astype(np.float32)), "hand weighted send"
+    s64, a64, send = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C, mean=True)
+    assert np.array_equal(s64.reshape(R, S, -1), d["mean"]), "hand mean64"
+    assert np.array_equal(send.reshape(R, S, -1), d["mean"].astype(np.float32)), "hand mean"
     fl = oracle.flags(B, R, C, 1, lib=lib)
     assert fl.tolist() == d["flags"], "hand flags"
 
@@ -233,6 +237,67 @@ def pin_torch_embedding_bag(lib):
         assert np.all(np.abs(send.astype(np.float64) - ref) <= 2.0 ** -24 * np.abs(ref) + 1e-12)
 
 
+def pin_mean_closed_forms(lib):
+    """Mean pooling: a bag of identical rows has that row as its mean for any
+    length; a single-row bag is the row itself; an empty bag is zero;
+    integer tables give the exact rational sum / L rounded once (compared
+    with Python fractions)."""
+    rng = np.random.default_rng(17)
+    T, B, R, C = 2, 24, 3, 4
+    rows, dims = [6, 50], [4, 12]
+    const = [np.repeat(rng.standard_normal((1, dims[t])).astype(np.float32), rows[t], axis=0) for t in range(T)]
+    off, idx = _random_bags(rng, T, B, rows, 60, allow_empty=True)
+    s64, a64, send = _pool(lib, const, 0, dims, idx, off, None, B, R, C, mean=True)
+    col = 0
+    for t in range(T):
+        for b in range(B):
+            L = off[t * B + b + 1] - off[t * B + b]
+            want = const[t][0].astype(np.float64) if L else np.zeros(dims[t])
+            assert np.array_equal(s64[b, col:col + dims[t]], want), (t, b, L)
+            assert np.array_equal(send[b, col:col + dims[t]], want.astype(np.float32))
+            assert np.array_equal(a64[b, col:col + dims[t]], np.abs(want))
+        col += dims[t]
+    ints = [rng.integers(-8, 9, size=(rows[t], dims[t])) for t in range(T)]
+    tabs = [x.astype(np.float32) for x in ints]
+    s64, _, send = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C, mean=True)
+    col = 0
+    for t in range(T):
+        for b in range(B):
+            ks = range(off[t * B + b], off[t * B + b + 1])
+            for j in range(dims[t]):
+                want = (fractions.Fraction(sum(int(ints[t][idx[k]][j]) for k in ks), len(ks)) if len(ks)
+                        else fractions.Fraction(0))
+                assert s64[b, col + j] == float(want), (t, b, j)
+        col += dims[t]
+    single = np.arange(T * B + 1, dtype=np.int64)
+    sidx = np.concatenate([rng.integers(0, rows[t], size=B) for t in range(T)]).astype(np.int32)
+    _, _, send = _pool(lib, tabs, 0, dims, sidx, single, None, B, R, C, mean=True)
+    col = 0
+    for t in range(T):
+        assert np.array_equal(send[:, col:col + dims[t]], tabs[t][sidx[t * B:(t + 1) * B]])
+        col += dims[t]
+
+
+def pin_torch_embedding_bag_mean(lib):
+    """F.embedding_bag(mode='mean') per table in fp64, concatenated along the
+    feature axis (PyTorch also returns zeros for an empty bag)."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(19)
+    T, B, R, C = 3, 30, 5, 3
+    rows, dims = [80, 33, 64], [8, 16, 4]
+    tabs = [rng.standard_normal((rows[t], dims[t])).astype(np.float32) for t in range(T)]
+    off, idx = _random_bags(rng, T, B, rows, 40, allow_empty=True)
+    s64, _, _ = _pool(lib, tabs, 0, dims, idx, off, None, B, R, C, mean=True)
+    parts = []
+    for t in range(T):
+        a, b = off[t * B], off[(t + 1) * B]
+        inp = torch.from_numpy(idx[a:b].astype(np.int64))
+        offs = torch.from_numpy((off[t * B:(t + 1) * B] - a).astype(np.int64))
+        parts.append(F.embedding_bag(inp, torch.from_numpy(tabs[t].astype(np.float64)), offs, mode="mean").numpy())
+    assert np.allclose(s64, np.concatenate(parts, axis=1), rtol=1e-12, atol=1e-12)
+
+
 def pin_validation(lib):
     """Inputs outside the definition are rejected with the documented code."""
     tabs = [np.zeros((4, 4), dtype=np.float32)]
@@ -262,7 +327,14 @@ def pin_validation(lib):
             assert msg in str(e), (msg, e)
         else:
             raise AssertionError(msg)
+    try:
+        _pool(lib, tabs, 0, [4], idx, off, np.ones(4, dtype=np.float32), 4, 2, 1, mean=True)
+    except oracle.OracleError as e:
+        assert "bad arguments" in str(e)
+    else:
+        raise AssertionError("mean pooling with weights accepted")
 
 
 ALL_PINS = [pin_hand, pin_integer_exact, pin_ones_and_weights, pin_row_coded, pin_placement,
-            pin_fp16_decode, pin_bf16_decode, pin_fp16_pool, pin_torch_embedding_bag, pin_validation]
+            pin_fp16_decode, pin_bf16_decode, pin_fp16_pool, pin_torch_embedding_bag, pin_mean_closed_forms,
+            pin_torch_embedding_bag_mean, pin_validation]

@@ -16,8 +16,8 @@ def test_pin(oracle_lib, pin):
 
 def test_brute_matches_hand():
     d = hand.load()
-    for key, w in (("sum", None), ("wsum", d["weights"])):
-        got = brute.pool(d["tables"], d["indices"], d["offsets"], w, d["B"], d["R"])
+    for key, w, mean in (("sum", None, False), ("wsum", d["weights"], False), ("mean", None, True)):
+        got = brute.pool(d["tables"], d["indices"], d["offsets"], w, d["B"], d["R"], mean=mean)
         assert np.array_equal(np.array(got), d[key])
     assert [f for row in brute.flags(d["B"], d["R"], d["C"], 1) for f in row] == d["flags"]
 
@@ -29,10 +29,10 @@ def test_brute_matches_c_random(oracle_lib):
     tabs = [rng.standard_normal((rows[t], dims[t])).astype(np.float32) for t in range(T)]
     off, idx = oracle_pins._random_bags(rng, T, B, rows, 9, allow_empty=True)
     w = rng.random(off[-1], dtype=np.float32)
-    for weights in (None, w):
-        s64, _, send = oracle.pool(tabs, 0, dims, idx, off, weights, B, R, C, lib=oracle_lib)
+    for weights, mean in ((None, False), (w, False), (None, True)):
+        s64, _, send = oracle.pool(tabs, 0, dims, idx, off, weights, B, R, C, lib=oracle_lib, mean=mean)
         ref = np.array(brute.pool([t.tolist() for t in tabs], idx.tolist(), off.tolist(),
-                                  None if weights is None else weights.tolist(), B, R))
+                                  None if weights is None else weights.tolist(), B, R, mean=mean))
         assert np.array_equal(s64, ref.reshape(B, -1))
 
 
@@ -42,12 +42,13 @@ def test_sampled_matches_c(oracle_lib, base):
     operations in the same order) on small versions of every workload."""
     w = scaled(base, rows=300, B=base.R * base.C, T=min(base.T, 8))
     inp = make_inputs(w)
-    s64, a64, send = oracle.pool_inputs(inp, lib=oracle_lib)
     bags = sampled.sample_bags(w, 40)
-    for t, b, row, col, s, a in sampled.pool_bags(inp, bags):
-        D = w.dims[t]
-        assert np.array_equal(s64[row, col:col + D], s), (t, b)
-        assert np.array_equal(a64[row, col:col + D], a), (t, b)
+    for mean in ((False, True) if inp.weights is None else (False,)):
+        s64, a64, send = oracle.pool_inputs(inp, lib=oracle_lib, mean=mean)
+        for t, b, row, col, s, a in sampled.pool_bags(inp, bags, mean=mean):
+            D = w.dims[t]
+            assert np.array_equal(s64[row, col:col + D], s), (t, b)
+            assert np.array_equal(a64[row, col:col + D], a), (t, b)
 
 
 def test_fp32_summation_within_tolerance():

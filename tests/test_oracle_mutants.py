@@ -27,6 +27,8 @@ MUTANTS = {
     "bf16_shift": ("uint32_t bits = (uint32_t)h << 16;", "uint32_t bits = (uint32_t)h << 15;"),
     "no_range_check": ("if (indices[k] < 0 || (int64_t)indices[k] >= rows[t]) return OR_BAD_INDEX;", ""),
     "flags_off_by_one": ("flags[r * nC + c] = epoch;", "flags[r * nC + c] = epoch + (c == 0);"),
+    "mean_not_divided": ("          sum /= (double)(hi - lo);\n", ""),
+    "mean_divides_by_l_plus_one": ("          sum /= (double)(hi - lo);", "          sum /= (double)(hi - lo + 1);"),
     "round_down": ("if (J->send) J->send[out + j] = (float)sum;", "if (J->send) J->send[out + j] = (float)floor(sum);"),
 }
 
