@@ -99,7 +99,7 @@ def hbm_probe(nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9, ms
 
 
-def cpu_baseline(w, inp, bytes_fn, max_tables=None, min_seconds=10.0):
+def cpu_baseline(w, inp, bytes_fn, max_tables=None, min_seconds=10.0, mean=False):
     """The CPU oracle timed on this host's cores over the first tables of the
     same workload (all B samples of each)."""
     import numpy as np
@@ -127,7 +127,7 @@ def cpu_baseline(w, inp, bytes_fn, max_tables=None, min_seconds=10.0):
     while len(times) < 3 or sum(times) < min_seconds:
         t0 = time.time()
         oracle.pool(tables, w.dtype, sub.dims, idx, off, wts, w.B, w.R, w.C, nthreads=cores,
-                    want_abs=False, want_sum=True, want_send=True)
+                    want_abs=False, want_sum=True, want_send=True, mean=mean)
         times.append(time.time() - t0)
     med = sorted(times)[len(times) // 2]
     cpu_model = ""
@@ -174,7 +174,9 @@ def e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, consumer_first, p
     return round(1e3 * sorted(times)[len(times) // 2], 2) if times else None
 
 
-def run_workload(name, steps, warmup, with_cpu, profile):
+def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
+    import dataclasses
+
     import numpy as np
     import torch
 
@@ -185,11 +187,17 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     w = synth.FULL[name]
     t0 = time.time()
     inp = synth.make_inputs(w)
+    if mean:
+        # mean pooling takes no weights: the same bags, unweighted
+        w = w.with_(weighted=False)
+        inp = dataclasses.replace(inp, w=w, weights=None)
     log(f"[{name}] inputs generated in {time.time() - t0:.1f} s (nnz={inp.nnz})")
     dev = sdev.to_device(inp)
     torch.cuda.synchronize()
     alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None)
-    opts = PLAN_OPTS.get(name, {})
+    opts = dict(PLAN_OPTS.get(name, {}))
+    if mean:
+        opts["pooling_mode"] = 1
     plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **opts)
     send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
     recv = torch.empty_like(send)
@@ -230,6 +238,7 @@ def run_workload(name, steps, warmup, with_cpu, profile):
         "config": {"workload": name, "tables": w.T, "rows": w.rows[0], "dims": sorted(set(w.dims)),
                    "storage": {0: "f32", 1: "f16", 2: "bf16"}[w.dtype], "global_batch": w.B,
                    "bag_lengths": w.lengths, "indices": w.indices, "weighted": w.weighted,
+                   "pooling": "mean" if mean else "sum",
                    "destinations": w.R, "slice_samples": w.C, "parallelism": "1 GPU, R logical destinations"},
         "fused_us": round(fused_ms * 1e3, 2),
         "unfused_us": round(unfused_ms * 1e3, 2),
@@ -272,7 +281,7 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None,
                        "kernel": "fused_pool_kernel"}
-    tr = traffic_record(name)
+    tr = None if mean else traffic_record(name)
     if tr:
         out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
     out["paper_context"] = PAPER_CONTEXT
@@ -280,7 +289,7 @@ def run_workload(name, steps, warmup, with_cpu, profile):
     torch.cuda.empty_cache()
     if with_cpu:
         log(f"[{name}] timing the CPU oracle")
-        out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes)
+        out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes, mean=mean)
     return out
 
 
@@ -445,6 +454,7 @@ def main():
     ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--occupancy", action="store_true", help="persistent-grid occupancy sweep of the fused kernel")
     ap.add_argument("--timeline", action="store_true", help="per-slice release / drain times, both slice orders")
+    ap.add_argument("--mean", action="store_true", help="mean pooling (the same bags without weights)")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -469,7 +479,8 @@ def main():
         return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:
-        out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile)
+        out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile,
+                           mean=a.mean)
         print(json.dumps(out), flush=True)
     return 0
 

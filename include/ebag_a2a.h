@@ -21,7 +21,9 @@
  *  int64 entries, offsets[0] == 0, non-decreasing; indices are int32 in
  *  [0, rows_t).  An empty bag pools to a zero vector; repeated indices count
  *  with multiplicity.  weights (optional) are fp32, one per index: the bag
- *  value is sum_k w_k * row_k (plain sum when weights == NULL).
+ *  value is sum_k w_k * row_k (plain sum when weights == NULL).  A plan
+ *  created with pooling_mode = 1 pools the mean instead: the sum divided by
+ *  the bag length (weights must then be NULL).
  *
  *  Destinations: the batch is split into R contiguous parts of S = B / R
  *  samples, the first to destination 0 (Sec. III-A, worked example).  Pooled
@@ -50,8 +52,9 @@
  * before anything is enqueued; ebag_a2a_last_error() returns a message for
  * the calling thread's most recent failure.  Preconditions that are not
  * checked on the host (index range, offset monotonicity) are checked in the
- * kernels when the plan was created with check_indices = 1; a bad bag is then
- * skipped (pooled as zeros) and reported by ebag_a2a_status().
+ * kernels when the plan was created with check_indices = 1: rows with an
+ * out-of-range index are skipped, a bag whose offsets are invalid is pooled
+ * as zeros, and the first such bag is reported by ebag_a2a_status_ex().
  */
 #ifndef EBAG_A2A_H
 #define EBAG_A2A_H
@@ -94,6 +97,10 @@ typedef struct ebag_a2a_opts {
   int32_t stream_rows;         /* 1 (default): table rows are read with non-temporal loads (no reuse expected);
                                   0: cached loads (skewed index distributions with hot rows) */
   int64_t consume_timeout_us;  /* consumer gives up after this long (default 5,000,000 us) */
+  int32_t pooling_mode;        /* 0 (default): sum (weighted sum when weights are given); 1: mean -- the
+                                  bag's sum divided by its length L, zeros for an empty bag; takes no weights
+                                  (the sum / mean modes of the original pooling kernel, Sec. III-A) */
+  int32_t reserved;            /* must be 0 */
 } ebag_a2a_opts_t;
 
 /* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */
@@ -122,7 +129,8 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
  * its C*T bags is stored.  Slices complete progressively in slice order.
  *   tables: HOST array of T device pointers (16-byte aligned).
  *   indices, offsets, weights: device arrays as described above.
- *   B > 0, R > 0, B % R == 0, (B / R) % C == 0, B <= max_batch, R <= max_ranks.
+ *   B > 0, R > 0, B % R == 0, (B / R) % C == 0, B <= max_batch, R <= max_ranks;
+ *   weights == NULL when the plan pools means.
  *   send_buf: device fp32 [B * sum(D)], 16-byte aligned.  flags: device
  *   uint32 [B / C].
  */

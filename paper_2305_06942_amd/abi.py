@@ -32,6 +32,8 @@ class Opts(ctypes.Structure):
         ("consumer_wgs", ctypes.c_int32),
         ("stream_rows", ctypes.c_int32),
         ("consume_timeout_us", ctypes.c_int64),
+        ("pooling_mode", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
     ]
 
 

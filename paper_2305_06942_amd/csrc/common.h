@@ -63,6 +63,8 @@ struct PoolArgs {
   int32_t waves;              // wavefronts per workgroup (blockDim.x / 64)
   int32_t out_floats;         // LDS output buffer of the fast path: K x max dim
   int32_t stream_rows;        // 1: table rows loaded non-temporally
+  int32_t mean;               // 1: mean pooling (sum / bag length)
+  int32_t pad;
 };
 
 struct RepackArgs {

@@ -161,13 +161,17 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.stream_rows < 0 || o.stream_rows > 1) return fail(EBAG_EINVAL, "stream_rows must be 0 or 1");
   if (o.consumer_wgs < 1) return fail(EBAG_EINVAL, "consumer_wgs must be >= 1");
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
+  if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
+  if (o.reserved != 0) return fail(EBAG_EINVAL, "reserved option field must be 0");
   return EBAG_OK;
 }
 
 // Validation shared by both forwards; fills the slice order.
 int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32_t* indices, const int64_t* offsets,
-                  int64_t B, int32_t R, const float* send_buf, const uint32_t* flags, SliceOrder* so) {
+                  const float* weights, int64_t B, int32_t R, const float* send_buf, const uint32_t* flags,
+                  SliceOrder* so) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (weights && h->opts.pooling_mode == 1) return fail(EBAG_EINVAL, "mean pooling takes no weights");
   if (!tables) return fail(EBAG_EINVAL, "null table pointer array");
   if (!offsets || !send_buf || !flags) return fail(EBAG_EINVAL, "null offsets, send_buf or flags");
   if (!indices) return fail(EBAG_EINVAL, "null indices");
@@ -240,6 +244,7 @@ void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_
   a->waves = h->opts.waves_per_wg;
   a->out_floats = K * max_dim;
   a->stream_rows = h->opts.stream_rows;
+  a->mean = h->opts.pooling_mode == 1;
 }
 
 // The fast pooling kernels handle tables below 4 GiB (32-bit buffer offsets)
@@ -390,7 +395,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
                      const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
                      hipStream_t stream) {
   SliceOrder so;
-  int rc = check_forward(h, tables, indices, offsets, B, R, send_buf, flags, &so);
+  int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
   rc = sync_tables(h, tables, stream);
   if (rc) return rc;
@@ -408,7 +413,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
                              const int64_t* offsets, const float* weights, int64_t B, int32_t R,
                              float* send_buf, uint32_t* flags, hipStream_t stream) {
   SliceOrder so;
-  int rc = check_forward(h, tables, indices, offsets, B, R, send_buf, flags, &so);
+  int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
   rc = sync_tables(h, tables, stream);
   if (rc) return rc;

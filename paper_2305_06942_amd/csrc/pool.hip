@@ -73,6 +73,17 @@ template <> struct Widen<EBF16> {
   }
 };
 
+// Mean pooling: divide the bag's pooled sum by its length (div > 0; an IEEE
+// division, so an exact fp32 sum gives the correctly rounded mean).
+template <int EPV>
+__device__ __forceinline__ void divide(float* acc, int div) {
+  if (div > 0) {
+    const float d = (float)div;
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) acc[e] = acc[e] / d;
+  }
+}
+
 // LDS written by some lanes of a wave and read by others: keep the compiler
 // from reordering across this point and wait for the LDS writes.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -210,7 +221,7 @@ template <class E, int U, bool WT>
 __device__ __forceinline__ bool pool_bag_generic(const char* __restrict__ tab, const TabMeta& m,
                                                  const int32_t* __restrict__ idx, const float* __restrict__ wts,
                                                  int64_t lo, int L, int32_t* lds_i, float* lds_w, int lane,
-                                                 int check, float* __restrict__ orow, bool sc1) {
+                                                 int check, float* __restrict__ orow, bool sc1, int div) {
   constexpr int EPV = E::EPV;
   bool bad = false;
   for (int cb = 0; cb < m.vecs; cb += 64) {
@@ -255,6 +266,7 @@ __device__ __forceinline__ bool pool_bag_generic(const char* __restrict__ tab, c
       }
       wave_lds_sync();
     }
+    divide<EPV>(acc, div);
     if (act) {
       const __amdgpu_buffer_rsrc_t rs = row_rsrc(orow, m.dim * 4);
 #pragma unroll
@@ -272,12 +284,13 @@ __device__ __forceinline__ bool pool_bag_generic(const char* __restrict__ tab, c
 // of lane v's 32 bytes (every lane holds the total after the xor butterfly).
 template <int EPV>
 __device__ __forceinline__ void reduce_store(float* acc, int vs, int lane, float* __restrict__ orow, int dim,
-                                             bool sc1) {
+                                             bool sc1, int div) {
   const int V = 1 << vs;
   for (int msk = 32; msk >= V; msk >>= 1) {
 #pragma unroll
     for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], msk);
   }
+  divide<EPV>(acc, div);
   const int g = lane >> vs;
   const int v = lane & (V - 1);
   const __amdgpu_buffer_rsrc_t rs = row_rsrc(orow, dim * 4);
@@ -327,14 +340,16 @@ __device__ __forceinline__ TabMeta load_meta(const TabMeta* p) {
 }
 
 // Combine the G row groups and write the bag's pooled row (dim floats) into
-// the workgroup's LDS output buffer (lanes of group 0, EPV floats each).
+// the workgroup's LDS output buffer (lanes of group 0, EPV floats each);
+// div > 0: mean pooling over div rows.
 template <int EPV>
-__device__ __forceinline__ void reduce_to_lds(float* acc, int vs, int lane, float* lrow) {
+__device__ __forceinline__ void reduce_to_lds(float* acc, int vs, int lane, float* lrow, int div) {
   const int V = 1 << vs;
   for (int msk = 32; msk >= V; msk >>= 1) {
 #pragma unroll
     for (int e = 0; e < EPV; ++e) acc[e] += __shfl_xor(acc[e], msk);
   }
+  divide<EPV>(acc, div);
   if ((lane >> vs) == 0) {
     float4* d = reinterpret_cast<float4*>(lrow + (lane & (V - 1)) * EPV);
 #pragma unroll
@@ -493,7 +508,7 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
               wave_lds_sync();
             }
           }
-          reduce_to_lds<EPV>(acc, m.vshift, lane, lds_out + (blk + i - b0) * m.dim);
+          reduce_to_lds<EPV>(acc, m.vshift, lane, lds_out + (blk + i - b0) * m.dim, a.mean ? L : 0);
         }
         if (all) wave_lds_sync();
       }
@@ -543,10 +558,10 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
                            : gather_p2<E, U, WT, false>(rl, m.vshift, m.rows, lds_i, lds_w, n, lane, acc);
             wave_lds_sync();
           }
-          reduce_store<EPV>(acc, m.vshift, lane, orow, m.dim, sc1);
+          reduce_store<EPV>(acc, m.vshift, lane, orow, m.dim, sc1, a.mean ? L : 0);
         } else {
           bad |= pool_bag_generic<E, U, WT>(tab, m, a.indices, a.weights, lo, L, lds_i, lds_w, lane, a.check, orow,
-                                            sc1);
+                                            sc1, a.mean ? L : 0);
         }
         if (a.check && __any(bad) && lane == 0) atomicMin(&a.status[ST_FIRST_BAD_BAG], (int32_t)(obase + b));
       }
