@@ -99,6 +99,54 @@ def hbm_probe(nbytes=4 << 30, reps=10):
     return 2 * nbytes / (ms * 1e-3) / 1e9, ms
 
 
+def gather_probe_gbs(row_bytes, nt=True, reps=5, buf_bytes=16 << 30, _cache={}):
+    """Read rate (GB/s) of the random-row probe: uniformly random rows of
+    row_bytes over a buf_bytes buffer, 16-byte loads, 8 in flight per lane --
+    the practical ceiling of a uniform gather of rows that wide."""
+    import torch
+    from synth import device as sdev
+    key = (row_bytes, nt)
+    if key in _cache:
+        return _cache[key]
+    buf = torch.empty(buf_bytes, dtype=torch.uint8, device="cuda")
+    grid = 8192
+    out = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+    nbytes = sdev.gather_probe(buf, row_bytes, 64, grid, out, nt=nt)
+    ms = time_launches(lambda: sdev.gather_probe(buf, row_bytes, 64, grid, out, nt=nt), reps, s)
+    del buf, out
+    _cache[key] = nbytes / (ms * 1e-3) / 1e9
+    return _cache[key]
+
+
+def probe_ceiling(w, lengths, weighted, nt):
+    """Time the fused kernel would take if every table's rows were gathered at
+    the probe's rate for their width and the other bytes moved at the probe's
+    widest-row rate; returns (ceiling GB/s of algorithmic bytes, us)."""
+    L = lengths.reshape(w.T, w.B).sum(axis=1)
+    us = 0.0
+    row_total = 0
+    for t in range(w.T):
+        rb = w.dims[t] * w.elt
+        nb = int(L[t]) * rb
+        row_total += nb
+        us += nb / gather_probe_gbs(rb, nt) / 1e3
+    alg = algorithmic_bytes(w, lengths, weighted)
+    us += (alg - row_total) / gather_probe_gbs(512, nt) / 1e3
+    return alg / (us * 1e-6) / 1e9, us
+
+
+def run_row_probe():
+    rows = []
+    for rb in (64, 128, 256, 512, 1024):
+        for nt in (True, False):
+            g = gather_probe_gbs(rb, nt)
+            row = {"row_bytes": rb, "nontemporal": nt, "gbs": round(g, 1), "rows_per_us": round(g * 1e3 / rb, 1)}
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+    return rows
+
+
 def cpu_baseline(w, inp, bytes_fn, max_tables=None, min_seconds=10.0, mean=False):
     """The CPU oracle timed on this host's cores over the first tables of the
     same workload (all B samples of each)."""
@@ -278,6 +326,10 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
     out["unique_row_gbs"] = round((alg - rows_alg + inp.unique_row_bytes()) / (fused_ms * 1e-3) / 1e9, 2)
     probe, _ = hbm_probe()
     out["hbm_copy_probe_gbs"] = round(probe, 1)
+    ceil_gbs, ceil_us = probe_ceiling(w, inp.lengths, inp.weights is not None, bool(opts.get("stream_rows", 1)))
+    out["random_row_probe_ceiling"] = {
+        "gbs": round(ceil_gbs, 1), "us": round(ceil_us, 1), "frac": round(out["value"] / ceil_gbs, 4),
+        "note": "uniform random rows of each table's width at the probe's measured rate; Zipf reuse can beat it"}
     out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None,
                        "kernel": "fused_pool_kernel"}
@@ -455,6 +507,7 @@ def main():
     ap.add_argument("--occupancy", action="store_true", help="persistent-grid occupancy sweep of the fused kernel")
     ap.add_argument("--timeline", action="store_true", help="per-slice release / drain times, both slice orders")
     ap.add_argument("--mean", action="store_true", help="mean pooling (the same bags without weights)")
+    ap.add_argument("--row-probe", action="store_true", help="random-row read rate by row width")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -476,6 +529,9 @@ def main():
         return 0
     if a.timeline:
         run_timeline(a.workload, a.warmup)
+        return 0
+    if a.row_probe:
+        run_row_probe()
         return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:

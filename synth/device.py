@@ -32,6 +32,9 @@ def load():
         lib.synth_fill.restype = ctypes.c_int
         lib.synth_copy.argtypes = [P, P, ctypes.c_int64, ctypes.c_int32, P]
         lib.synth_copy.restype = ctypes.c_int
+        lib.synth_gather_probe.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, P, P]
+        lib.synth_gather_probe.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -95,3 +98,17 @@ def copy(dst, src, nbytes: int, grid: int = 0, stream=None):
     rc = load().synth_copy(dst.data_ptr(), src.data_ptr(), nbytes, grid, s)
     if rc != 0:
         raise RuntimeError(f"synth_copy failed: {rc}")
+
+
+def gather_probe(buf, row_bytes: int, steps: int, grid: int, out, nt: bool = True, stream=None) -> int:
+    """Random-row read probe over the bytes of ``buf`` (see synth/fill.hip);
+    returns the bytes it reads."""
+    import torch
+    s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+    nbytes = buf.numel() * buf.element_size()
+    if out.numel() * out.element_size() < grid * 256 * 4:
+        raise ValueError("probe output too small")
+    rc = load().synth_gather_probe(buf.data_ptr(), nbytes, row_bytes, steps, grid, int(nt), out.data_ptr(), s)
+    if rc != 0:
+        raise RuntimeError(f"synth_gather_probe failed: {rc}")
+    return grid * 4 * steps * 1024

@@ -1,7 +1,9 @@
 // Device side of the seeded input generator: fills a table in place with the
 // counter-based value function (SplitMix64, Steele/Lea/Flood 2014) so that
-// 10^11-byte tables never cross PCIe, and a plain 16-byte copy kernel used as
-// an HBM bandwidth probe and as the byte-counter calibration for profiling.
+// 10^11-byte tables never cross PCIe, and two measurement kernels: a plain
+// 16-byte copy (HBM bandwidth probe and byte-counter calibration for
+// profiling) and a random-row read probe (the practical ceiling of a gather
+// of rows of a given width).
 //
 // The value function must match synth/gen.py bit for bit:
 //   u = splitmix64(seed ^ (row*dim + j)) >> 40
@@ -89,6 +91,35 @@ __global__ void copy_kernel(uint4* __restrict__ dst, const uint4* __restrict__ s
   for (; i < n16; i += stride) dst[i] = src[i];
 }
 
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+// Random-row reads: every wave reads `steps` x (64 / lanes-per-row) rows of
+// rb = 16 << lshift bytes at pseudo-random row numbers below nrows (16-byte
+// loads, rb / 16 lanes per row, 8 loads in flight per lane) and folds them
+// into one word per thread so the loads cannot be dropped.
+template <bool NT>
+__global__ __launch_bounds__(256) void gather_probe_kernel(const char* __restrict__ base, uint64_t nrows, int lshift,
+                                                           int steps, uint32_t* __restrict__ out) {
+  const int lane = threadIdx.x & 63;
+  const uint64_t wave = ((uint64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int sub = lane >> lshift;
+  const uint64_t col = (uint64_t)(lane & ((1 << lshift) - 1)) * 16;
+  const uint64_t rb = (uint64_t)16 << lshift;
+  u4v acc = {0u, 0u, 0u, 0u};
+  for (int s0 = 0; s0 < steps; s0 += 8) {
+    u4v r[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t row = splitmix64((wave << 32) ^ ((uint64_t)(s0 + u) << 8) ^ (uint64_t)sub) % nrows;
+      const u4v* p = reinterpret_cast<const u4v*>(base + row * rb + col);
+      r[u] = NT ? __builtin_nontemporal_load(p) : *p;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= r[u];
+  }
+  out[(uint64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -116,6 +147,26 @@ int synth_copy(void* dst, const void* src, int64_t bytes, int32_t grid, hipStrea
   if (n16 == 0) return 0;
   unsigned g = grid > 0 ? (unsigned)grid : 4096u;
   hipLaunchKernelGGL(copy_kernel, dim3(g), dim3(256), 0, stream, (uint4*)dst, (const uint4*)src, n16);
+  return (int)hipGetLastError();
+}
+
+// Random-row read probe over base[0:bytes): grid workgroups of 256 threads,
+// each wave reading steps x (1024 / row_bytes) rows of row_bytes (16..1024, a
+// power of two) at pseudo-random positions; nt = 1 uses non-temporal loads.
+// out: grid * 256 uint32 (device).  Bytes read = grid * 4 * steps * 1024.
+int synth_gather_probe(const void* base, int64_t bytes, int32_t row_bytes, int32_t steps, int32_t grid, int32_t nt,
+                       void* out, hipStream_t stream) {
+  int lshift = 0;
+  while ((16 << lshift) < row_bytes && lshift < 6) ++lshift;
+  if (!base || !out || (16 << lshift) != row_bytes || bytes < row_bytes || steps <= 0 || steps % 8 || grid <= 0)
+    return -1;
+  const uint64_t nrows = (uint64_t)bytes / (uint64_t)row_bytes;
+  if (nt)
+    hipLaunchKernelGGL(gather_probe_kernel<true>, dim3(grid), dim3(256), 0, stream, (const char*)base, nrows, lshift,
+                       steps, (uint32_t*)out);
+  else
+    hipLaunchKernelGGL(gather_probe_kernel<false>, dim3(grid), dim3(256), 0, stream, (const char*)base, nrows,
+                       lshift, steps, (uint32_t*)out);
   return (int)hipGetLastError();
 }
 

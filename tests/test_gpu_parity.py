@@ -208,3 +208,19 @@ def test_occupancy_query_and_full_persistent_grid():
         torch.cuda.synchronize()
         check_full(inp, send.cpu().numpy(), s64, a64)
         assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+
+
+def test_gather_probe_reads_in_bounds_rows():
+    """The random-row probe used by the benchmark: a buffer of identical
+    16-byte words folds to zero in every thread (an even number of loads per
+    lane), for every supported row width."""
+    import torch
+    buf = torch.full((1 << 22,), 0x01020304, dtype=torch.int32, device="cuda")
+    grid = 16
+    out = torch.full((grid * 256,), -1, dtype=torch.int32, device="cuda")
+    for rb in (16, 64, 128, 256, 512, 1024):
+        out.fill_(-1)
+        n = sdev.gather_probe(buf, rb, 16, grid, out, nt=(rb % 128 == 0))
+        torch.cuda.synchronize()
+        assert n == grid * 4 * 16 * 1024
+        assert int(out.abs().sum()) == 0
