@@ -48,7 +48,7 @@ def kernel_hash():
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(w, lengths, weighted):
+def algorithmic_bytes(w, lengths, weighted, n_flags=None):
     """Bytes the method itself must move for one forward: every gathered row,
     every index (+ weight), the CSR offsets, the fp32 output and one flag per
     slice."""
@@ -56,7 +56,8 @@ def algorithmic_bytes(w, lengths, weighted):
     L = lengths.reshape(w.T, w.B).sum(axis=1)  # indices per table
     rows = int(sum(int(L[t]) * w.dims[t] * w.elt for t in range(w.T)))
     nnz = int(L.sum())
-    return rows + 4 * nnz + (4 * nnz if weighted else 0) + 8 * (w.T * w.B + 1) + 4 * w.B * w.sum_dim + 4 * w.n_chunks
+    n_flags = w.n_chunks if n_flags is None else n_flags
+    return rows + 4 * nnz + (4 * nnz if weighted else 0) + 8 * (w.T * w.B + 1) + 4 * w.B * w.sum_dim + 4 * n_flags
 
 
 def traffic_record(workload):
@@ -222,7 +223,7 @@ def e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, consumer_first, p
     return round(1e3 * sorted(times)[len(times) // 2], 2) if times else None
 
 
-def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
+def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=False):
     import dataclasses
 
     import numpy as np
@@ -242,14 +243,17 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
     log(f"[{name}] inputs generated in {time.time() - t0:.1f} s (nnz={inp.nnz})")
     dev = sdev.to_device(inp)
     torch.cuda.synchronize()
-    alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None)
     opts = dict(PLAN_OPTS.get(name, {}))
     if mean:
         opts["pooling_mode"] = 1
+    if per_table:
+        opts["slice_granule"] = 1
+    n_flags = w.n_chunks * (w.T if per_table else 1)
+    alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None, n_flags)
     plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **opts)
     send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
     recv = torch.empty_like(send)
-    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
     epoch = [0]
     stream = torch.cuda.current_stream()
 
@@ -287,6 +291,7 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
                    "storage": {0: "f32", 1: "f16", 2: "bf16"}[w.dtype], "global_batch": w.B,
                    "bag_lengths": w.lengths, "indices": w.indices, "weighted": w.weighted,
                    "pooling": "mean" if mean else "sum",
+                   "slices": "per table" if per_table else "all tables",
                    "destinations": w.R, "slice_samples": w.C, "parallelism": "1 GPU, R logical destinations"},
         "fused_us": round(fused_ms * 1e3, 2),
         "unfused_us": round(unfused_ms * 1e3, 2),
@@ -317,11 +322,11 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
     # overlap evidence from device timestamps
     tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
     e2e_us(tplan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, 0)
-    rel, drn, tpu = tplan.trace(w.n_chunks)
+    rel, drn, tpu = tplan.trace(n_flags)
     out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
     out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
     out["median_drain_lag_us"] = round(float(np.median(drn.astype(np.int64) - rel.astype(np.int64))) / tpu, 2)
-    out["n_slices"] = w.n_chunks
+    out["n_slices"] = n_flags
     rows_alg = int(sum(int(inp.lengths.reshape(w.T, w.B)[t].sum()) * w.dims[t] * w.elt for t in range(w.T)))
     out["unique_row_gbs"] = round((alg - rows_alg + inp.unique_row_bytes()) / (fused_ms * 1e-3) / 1e9, 2)
     probe, _ = hbm_probe()
@@ -333,7 +338,7 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False):
     out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                        "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None,
                        "kernel": "fused_pool_kernel"}
-    tr = None if mean else traffic_record(name)
+    tr = None if (mean or per_table) else traffic_record(name)
     if tr:
         out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
     out["paper_context"] = PAPER_CONTEXT
@@ -508,6 +513,7 @@ def main():
     ap.add_argument("--timeline", action="store_true", help="per-slice release / drain times, both slice orders")
     ap.add_argument("--mean", action="store_true", help="mean pooling (the same bags without weights)")
     ap.add_argument("--row-probe", action="store_true", help="random-row read rate by row width")
+    ap.add_argument("--per-table-slices", action="store_true", help="a ready flag per (slice, table)")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -536,7 +542,7 @@ def main():
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:
         out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile,
-                           mean=a.mean)
+                           mean=a.mean, per_table=a.per_table_slices)
         print(json.dumps(out), flush=True)
     return 0
 

@@ -35,7 +35,11 @@
  *  Slices ("chunks"): slice (r, c) is the C samples r*S + c*C ..
  *  r*S + (c+1)*C - 1 of destination r for all T tables -- a contiguous block
  *  of C * sum(D) floats.  flags has R * (S / C) uint32 entries, slice (r, c)
- *  at r * (S / C) + c (equivalently the global slice g = b / C).
+ *  at r * (S / C) + c (equivalently the global slice g = b / C).  With
+ *  slice_granule = 1 each slice is split per table: flag (g, t) covers the C
+ *  pooled vectors of table t in slice g (columns off_t .. off_t + D_t of C
+ *  consecutive rows), flags has T * (B / C) entries and (g, t) is at
+ *  g * T + t.  "Flag index" below means this index.
  *
  *  Flags are epochs: the caller zeroes the flag array once; every completed
  *  forward adds exactly 1 to every flag of the batch with release semantics
@@ -92,7 +96,7 @@ typedef struct ebag_a2a_opts {
   int32_t self_rank;           /* the destination whose slices stay local (chunk_order == 1) */
   int32_t trace;               /* 1: record a device timestamp at every slice release and drain */
   int32_t check_indices;       /* 1: kernels check offsets/indices, skip and report bad bags */
-  int32_t debug_suppress_flag; /* >= 0: never publish this slice's flag (failure-path tests); -1 off */
+  int32_t debug_suppress_flag; /* >= 0: never publish the flag with this index (failure-path tests); -1 off */
   int32_t consumer_wgs;        /* single-wave workgroups of the consumer kernel (default 512) */
   int32_t stream_rows;         /* 1 (default): table rows are read with non-temporal loads (no reuse expected);
                                   0: cached loads (skewed index distributions with hot rows) */
@@ -100,7 +104,9 @@ typedef struct ebag_a2a_opts {
   int32_t pooling_mode;        /* 0 (default): sum (weighted sum when weights are given); 1: mean -- the
                                   bag's sum divided by its length L, zeros for an empty bag; takes no weights
                                   (the sum / mean modes of the original pooling kernel, Sec. III-A) */
-  int32_t reserved;            /* must be 0 */
+  int32_t slice_granule;       /* 0 (default): a flag per (destination, C samples) for all T tables;
+                                  1: a flag per (destination, C samples, table) -- the paper's per-table
+                                  slice (Sec. III-A); see "Slices" above */
 } ebag_a2a_opts_t;
 
 /* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */
@@ -132,7 +138,7 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
  *   B > 0, R > 0, B % R == 0, (B / R) % C == 0, B <= max_batch, R <= max_ranks;
  *   weights == NULL when the plan pools means.
  *   send_buf: device fp32 [B * sum(D)], 16-byte aligned.  flags: device
- *   uint32 [B / C].
+ *   uint32 [B / C] ([T * B / C] with slice_granule = 1).
  */
 int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices, const int64_t* offsets,
                      const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
@@ -151,10 +157,11 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
 
 /*
  * Receiver side (Sec. III-A, "Book-keeping Flags"): each slice is split
- * into pieces of up to 32 KiB; each consumer workgroup (one wavefront) owns a
- * distinct subset of pieces, polls the slice's flag until it reaches
- * expected_epoch, then copies the piece from send_buf to recv_buf (same
- * layout and size).  Meant to run on a second
+ * into pieces of up to 32 KiB (with slice_granule = 1: one piece per
+ * per-table slice, C rows of D_t floats); each consumer workgroup (one
+ * wavefront) owns a distinct subset of pieces, polls the slice's flag until
+ * it reaches expected_epoch, then copies the piece from send_buf to recv_buf
+ * (same layout and size).  Meant to run on a second
  * stream concurrently with a forward.  Enqueue it after the forward it
  * waits for: streams may share a hardware queue, and a consumer queued ahead
  * of its producer on the same queue can only time out.  Polling is bounded
@@ -167,15 +174,15 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
 /*
  * Synchronise the device and read the plan's status word.
  *   timed_out: 1 if a consumer gave up waiting, else 0.
- *   first_missing_flag: lowest slice index a consumer timed out on, else -1.
+ *   first_missing_flag: lowest flag index a consumer timed out on, else -1.
  * Returns EBAG_OK, or EBAG_ETIMEOUT when timed_out is set.
  */
 int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_flag);
 
 /*
- * Extended status: out[0] timed_out, out[1] first missing slice (-1 none),
- * out[2] slices whose flag was seen above the expected epoch (double
- * publication), out[3] first bad bag t*B+b found by check_indices (-1 none).
+ * Extended status: out[0] timed_out, out[1] first missing flag index (-1
+ * none), out[2] flags seen above the expected epoch (double publication),
+ * out[3] first bad bag t*B+b found by check_indices (-1 none).
  */
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]);
 
@@ -185,9 +192,10 @@ int ebag_a2a_reset(ebag_a2a_t h);
 
 /*
  * Copy the per-slice timestamps of the most recent traced forward/consume
- * (plan created with trace = 1) to host arrays of n entries:
- * release_ticks[g] when slice g's flag was released, drain_ticks[g] when a
- * consumer finished copying it (0 = not recorded).  Ticks are the device's
+ * (plan created with trace = 1) to host arrays of n entries, one per flag
+ * index (n at most the flag count of max_batch): release_ticks[f] when flag
+ * f was released, drain_ticks[f] when a consumer finished copying its slice
+ * (0 = not recorded).  Ticks are the device's
  * constant wall clock; *ticks_per_us receives its rate.  Synchronous.
  */
 int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks, int64_t n,

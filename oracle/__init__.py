@@ -53,7 +53,7 @@ def load(path: str = LIB):
     lib.oracle_pool.restype = ctypes.c_int
     lib.oracle_validate.argtypes = [i32, P, P, P, i64, P, i64, i32, i32]
     lib.oracle_validate.restype = ctypes.c_int
-    lib.oracle_flags.argtypes = [i64, i32, i32, ctypes.c_uint32, P, i64]
+    lib.oracle_flags.argtypes = [i64, i32, i32, i32, ctypes.c_uint32, P, i64]
     lib.oracle_flags.restype = ctypes.c_int
     lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
     lib.oracle_half_to_double.restype = ctypes.c_double
@@ -112,13 +112,15 @@ def pool_inputs(inp, nthreads=None, **kw):
                 nthreads=nthreads, **kw)
 
 
-def flags(B, R, C, epoch, lib=None):
+def flags(B, R, C, epoch, lib=None, per_slice=1):
+    """Expected flags after ``epoch`` forwards; per_slice = T for per-table
+    slices (flag (g, t) at g * T + t)."""
     lib = lib or load()
     if B <= 0 or R <= 0 or C <= 0 or B % R or (B // R) % C:
         raise OracleError("B % R or S % C not zero")
-    n = R * ((B // R) // C)
+    n = R * ((B // R) // C) * per_slice
     out = np.empty(n, dtype=np.uint32)
-    rc = lib.oracle_flags(B, R, C, epoch, out.ctypes.data, n)
+    rc = lib.oracle_flags(B, R, C, per_slice, epoch, out.ctypes.data, n)
     if rc != 0:
         raise OracleError(f"oracle_flags: {ERRORS.get(rc, rc)}")
     return out

@@ -26,9 +26,10 @@
  *
  *   Ready flags (Sec. III-A, "Book-keeping Flags"): one flag per slice; a
  *   slice here is C consecutive samples of one destination for all tables, so
- *   destination r has S / C slices and flag (r, c) is at r * (S / C) + c.
- *   After `epoch` complete forwards from a zeroed array every flag equals
- *   `epoch`.
+ *   destination r has S / C slices and flag (r, c) is at r * (S / C) + c --
+ *   or, with per-table slices, one flag per (slice, table) at
+ *   (r * (S / C) + c) * T + t.  After `epoch` complete forwards from a zeroed
+ *   array every flag equals `epoch`.
  *
  * Readings of points the paper leaves open: empty bags give zeros; repeated
  * indices count with multiplicity; out-of-range indices, non-monotone offsets,
@@ -194,13 +195,17 @@ int oracle_pool(int32_t T, const void* const* tables, const int64_t* rows, const
   return OR_OK;
 }
 
-/* Step 4: the ready flags after `epoch` complete forwards: R * (S / C)
- * entries, slice (r, c) at r * (S / C) + c, each equal to epoch. */
-int oracle_flags(int64_t B, int32_t R, int32_t C, uint32_t epoch, uint32_t* flags, int64_t n_flags) {
+/* Step 4: the ready flags after `epoch` complete forwards.  per_slice = 1:
+ * R * (S / C) entries, slice (r, c) at r * (S / C) + c.  per_slice = T
+ * (the per-table slices of Sec. III-A): each slice is split per table and
+ * (r, c, t) is at (r * (S / C) + c) * T + t.  Every entry equals epoch. */
+int oracle_flags(int64_t B, int32_t R, int32_t C, int32_t per_slice, uint32_t epoch, uint32_t* flags,
+                 int64_t n_flags) {
   if (B <= 0 || R <= 0 || C <= 0 || B % R || (B / R) % C) return OR_BAD_SPLIT;
   const int64_t S = B / R, nC = S / C;
-  if (n_flags != R * nC || !flags) return OR_BAD_ARGS;
+  if (per_slice <= 0 || n_flags != R * nC * per_slice || !flags) return OR_BAD_ARGS;
   for (int64_t r = 0; r < R; ++r)
-    for (int64_t c = 0; c < nC; ++c) flags[r * nC + c] = epoch;
+    for (int64_t c = 0; c < nC; ++c)
+      for (int32_t t = 0; t < per_slice; ++t) flags[(r * nC + c) * per_slice + t] = epoch;
   return OR_OK;
 }

@@ -33,7 +33,7 @@ class Opts(ctypes.Structure):
         ("stream_rows", ctypes.c_int32),
         ("consume_timeout_us", ctypes.c_int64),
         ("pooling_mode", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("slice_granule", ctypes.c_int32),
     ]
 
 
@@ -184,6 +184,10 @@ class Plan:
 
     def reset(self):
         _check(self._lib.ebag_a2a_reset(self._h))
+
+    def n_flags(self, B):
+        """Flag count of a forward over B samples (B / C, times T per-table)."""
+        return (B // self.C) * (self.T if self.opts.slice_granule == 1 else 1)
 
     def trace(self, n):
         import numpy as np

@@ -45,13 +45,13 @@ struct PoolArgs {
   const int64_t* offsets;
   const float* weights;       // nullptr for plain sum
   float* out;                 // fused: send buffer; unfused: [T][B][D_t] scratch
-  uint32_t* counters;         // [n_chunks] bags finished per slice (self-resetting)
-  uint32_t* flags;            // [n_chunks] epoch flags
+  uint32_t* counters;         // [n_flags] bags finished per flag's slice (self-resetting)
+  uint32_t* flags;            // [n_flags] epoch flags
   int32_t* status;            // plan status word
-  uint64_t* trace_release;    // [n_chunks] or nullptr
+  uint64_t* trace_release;    // [n_flags] or nullptr
   int64_t B;
   int64_t nruns;
-  int64_t suppress;           // slice whose flag is never released (-1: none)
+  int64_t suppress;           // flag index never released (-1: none)
   SliceOrder so;
   int32_t T;
   int32_t C;
@@ -64,7 +64,7 @@ struct PoolArgs {
   int32_t out_floats;         // LDS output buffer of the fast path: K x max dim
   int32_t stream_rows;        // 1: table rows loaded non-temporally
   int32_t mean;               // 1: mean pooling (sum / bag length)
-  int32_t pad;
+  int32_t per_table;          // 1: one flag / counter per (slice, table), index g * T + t
 };
 
 struct RepackArgs {
@@ -84,7 +84,7 @@ struct RepackArgs {
 struct PublishArgs {
   uint32_t* flags;
   uint64_t* trace_release;
-  int64_t n_chunks;
+  int64_t n_flags;
   int64_t suppress;
 };
 
@@ -94,13 +94,19 @@ struct ConsumeArgs {
   float* recv;
   int32_t* status;
   uint64_t* trace_drain;
+  const TabMeta* meta;        // per-table slices: column range of each table
+  const int32_t* tperm;       // per-table slices: production order of tables
   int64_t chunk_floats;       // C * sum D
-  int64_t piece_f4;           // float4s per work item
-  int64_t pieces;             // work items per slice
+  int64_t piece_f4;           // float4s per work item (whole-slice granule)
+  int64_t pieces;             // work items per slice (whole-slice granule)
   uint64_t timeout_ticks;
   SliceOrder so;
   uint32_t epoch;
   int32_t coherent_loads;     // 1: device-scope loads of slice data (no cache invalidation)
+  int32_t per_table;          // 1: one work item per (slice, table), flag g * T + t
+  int32_t T;
+  int32_t C;
+  int32_t sum_dim;
 };
 
 // Status word layout (int32[4]).

@@ -121,6 +121,7 @@ struct ebag_a2a_plan {
   std::vector<const void*> host_tables;  // last table pointers uploaded
   bool tables_valid = false;
   int64_t max_chunks = 0;
+  int64_t max_flags = 0;   // max_chunks, times T with per-table slices
   // device memory
   TabMeta* d_meta = nullptr;
   int32_t* d_tperm = nullptr;
@@ -162,7 +163,7 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.consumer_wgs < 1) return fail(EBAG_EINVAL, "consumer_wgs must be >= 1");
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
-  if (o.reserved != 0) return fail(EBAG_EINVAL, "reserved option field must be 0");
+  if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
   return EBAG_OK;
 }
 
@@ -245,6 +246,7 @@ void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_
   a->out_floats = K * max_dim;
   a->stream_rows = h->opts.stream_rows;
   a->mean = h->opts.pooling_mode == 1;
+  a->per_table = h->opts.slice_granule == 1;
 }
 
 // The fast pooling kernels handle tables below 4 GiB (32-bit buffer offsets)
@@ -347,6 +349,7 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   h->meta = meta;
   h->host_tables.assign(num_tables, nullptr);
   h->max_chunks = (max_batch + chunk_samples - 1) / chunk_samples;
+  h->max_flags = h->max_chunks * (o.slice_granule == 1 ? num_tables : 1);
 
 #define CREATE_TRY(call, what)                                                             \
   do {                                                                                     \
@@ -374,16 +377,16 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");
   CREATE_TRY(hipMemcpy(h->d_tperm, tperm.data(), sizeof(int32_t) * num_tables, hipMemcpyHostToDevice), "upload order");
   CREATE_TRY(hipMalloc((void**)&h->d_tables, sizeof(void*) * num_tables), "alloc table pointers");
-  CREATE_TRY(hipMalloc((void**)&h->d_counters, sizeof(uint32_t) * h->max_chunks), "alloc slice counters");
-  CREATE_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_chunks), "zero slice counters");
+  CREATE_TRY(hipMalloc((void**)&h->d_counters, sizeof(uint32_t) * h->max_flags), "alloc slice counters");
+  CREATE_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero slice counters");
   CREATE_TRY(hipMalloc((void**)&h->d_scratch, sizeof(float) * (size_t)max_batch * (size_t)sum_dim), "alloc scratch");
   CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
   CREATE_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "init status");
   if (o.trace) {
-    CREATE_TRY(hipMalloc((void**)&h->d_trace_release, sizeof(uint64_t) * h->max_chunks), "alloc trace");
-    CREATE_TRY(hipMalloc((void**)&h->d_trace_drain, sizeof(uint64_t) * h->max_chunks), "alloc trace");
-    CREATE_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
-    CREATE_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+    CREATE_TRY(hipMalloc((void**)&h->d_trace_release, sizeof(uint64_t) * h->max_flags), "alloc trace");
+    CREATE_TRY(hipMalloc((void**)&h->d_trace_drain, sizeof(uint64_t) * h->max_flags), "alloc trace");
+    CREATE_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_flags), "zero trace");
+    CREATE_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_flags), "zero trace");
   }
 #undef CREATE_TRY
   *out = h;
@@ -442,7 +445,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   PublishArgs pa;
   pa.flags = flags;
   pa.trace_release = h->opts.trace ? h->d_trace_release : nullptr;
-  pa.n_chunks = so.n_chunks;
+  pa.n_flags = so.n_chunks * (h->opts.slice_granule == 1 ? h->T : 1);
   pa.suppress = h->opts.debug_suppress_flag;
   e = launch_publish(pa, stream);
   if (e != hipSuccess) return hip_fail(e, "launch flag publication kernel");
@@ -473,12 +476,19 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   c.so.order = h->opts.chunk_order;
   c.epoch = expected_epoch;
   c.coherent_loads = h->opts.release_mode == 1;
-  // Work items of at most 32 KiB per slice.
+  c.per_table = h->opts.slice_granule == 1;
+  c.meta = h->d_meta;
+  c.tperm = h->d_tperm;
+  c.T = h->T;
+  c.C = h->C;
+  c.sum_dim = h->sum_dim;
+  // Work items: pieces of at most 32 KiB per slice, or one per (slice, table).
   const int64_t chunk_f4 = c.chunk_floats / 4;
   c.piece_f4 = chunk_f4 < 2048 ? chunk_f4 : 2048;
   c.pieces = (chunk_f4 + c.piece_f4 - 1) / c.piece_f4;
+  const int64_t items = c.so.n_chunks * (c.per_table ? h->T : c.pieces);
   int64_t grid = h->opts.consumer_wgs;
-  if (grid > c.so.n_chunks * c.pieces) grid = c.so.n_chunks * c.pieces;
+  if (grid > items) grid = items;
   hipError_t e = launch_consume(c, (int)grid, 64, stream);
   if (e != hipSuccess) return hip_fail(e, "launch consumer kernel");
   return EBAG_OK;
@@ -508,11 +518,11 @@ int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_fla
 int ebag_a2a_reset(ebag_a2a_t h) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
-  HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_chunks), "zero counters");
+  HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero counters");
   HIP_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "reset status");
   if (h->d_trace_release) {
-    HIP_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
-    HIP_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_chunks), "zero trace");
+    HIP_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_flags), "zero trace");
+    HIP_TRY(hipMemset(h->d_trace_drain, 0, sizeof(uint64_t) * h->max_flags), "zero trace");
   }
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   return EBAG_OK;
@@ -521,7 +531,7 @@ int ebag_a2a_reset(ebag_a2a_t h) {
 int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks, int64_t n, double* ticks_per_us) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
   if (!h->d_trace_release) return fail(EBAG_EINVAL, "plan was created without trace = 1");
-  if (n < 0 || n > h->max_chunks) return fail(EBAG_EINVAL, "n=%lld outside [0, %lld]", (long long)n, (long long)h->max_chunks);
+  if (n < 0 || n > h->max_flags) return fail(EBAG_EINVAL, "n=%lld outside [0, %lld]", (long long)n, (long long)h->max_flags);
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   if (release_ticks && n)
     HIP_TRY(hipMemcpy(release_ticks, h->d_trace_release, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");

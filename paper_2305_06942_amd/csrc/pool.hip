@@ -414,7 +414,8 @@ __device__ __forceinline__ void wait_stores_complete() { __builtin_amdgcn_s_wait
 constexpr int SEGW = 512;  // indices a wave stages at once for a block of bags
 
 // One workgroup per run: up to K consecutive samples of one table inside one
-// slice.  Wave w pools a contiguous block of the run's bags: it loads the
+// slice.  The counter it feeds is the slice's (target C * T bags) or, with
+// per-table slices, the (slice, table) pair's (target C bags).  Wave w pools a contiguous block of the run's bags: it loads the
 // block's CSR offsets with one vector load, stages the block's whole index
 // segment into its LDS slot when it fits (else bag by bag, SEG at a time),
 // then gathers, reduces and stores every bag.
@@ -526,8 +527,9 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
         if (FUSED) {
           if (a.release_mode == 1) wait_stores_complete();
           if (lane == 0)
-            release_slice(a.counters, a.flags, g, (uint32_t)nb, (uint32_t)a.C * (uint32_t)a.T, a.suppress,
-                          a.trace_release, a.release_mode);
+            release_slice(a.counters, a.flags, a.per_table ? g * a.T + t : g, (uint32_t)nb,
+                          a.per_table ? (uint32_t)a.C : (uint32_t)a.C * (uint32_t)a.T, a.suppress, a.trace_release,
+                          a.release_mode);
         }
       }
       // A persistent workgroup reuses the LDS output buffer for its next run.
@@ -570,8 +572,9 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
       if (a.release_mode == 1) wait_stores_complete();
       __syncthreads();
       if (threadIdx.x == 0)
-        release_slice(a.counters, a.flags, g, (uint32_t)nb, (uint32_t)a.C * (uint32_t)a.T, a.suppress,
-                      a.trace_release, a.release_mode);
+        release_slice(a.counters, a.flags, a.per_table ? g * a.T + t : g, (uint32_t)nb,
+                      a.per_table ? (uint32_t)a.C : (uint32_t)a.C * (uint32_t)a.T, a.suppress, a.trace_release,
+                      a.release_mode);
     }
   }
 }

@@ -29,11 +29,11 @@ __global__ __launch_bounds__(256) void repack_kernel(const RepackArgs a) {
 }
 
 // Unfused baseline, third step: after the repack kernel has ended (kernel
-// boundary = all its stores visible device-wide), every slice flag is bumped
-// at once -- the collective can only start once the whole batch is pooled.
+// boundary = all its stores visible device-wide), every flag is bumped at
+// once -- the collective can only start once the whole batch is pooled.
 __global__ __launch_bounds__(256) void publish_kernel(const PublishArgs a) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (g >= a.n_chunks) return;
+  if (g >= a.n_flags) return;
   if (a.trace_release) a.trace_release[g] = wall_clock64();
   if (g != a.suppress) __hip_atomic_fetch_add(&a.flags[g], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -41,64 +41,108 @@ __global__ __launch_bounds__(256) void publish_kernel(const PublishArgs a) {
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
 constexpr int kBufferWord3 = 0x00020000;  // raw buffer, 32-bit data format
 
-// Receiver (Sec. III-A, "Book-keeping Flags"): each slice is cut into pieces
-// and the single-wave workgroups take pieces in production order, so the
-// pieces of the slices that complete last are drained by many waves at once.
-// A wave polls the slice flag (relaxed device-scope loads with s_sleep
-// back-off, bounded by a wall-clock deadline), then copies its piece from
-// send to recv.  With coherent_loads the piece is read with device-scope
-// loads, which see the producer's device-scope stores without invalidating
-// this XCD's L2; otherwise an agent-scope acquire precedes plain loads.
+// Wait until flag f reaches the epoch (relaxed device-scope loads with
+// s_sleep back-off) or the wall-clock deadline passes.  Returns the value
+// seen, or records the timeout and returns false in *ok.
+__device__ __forceinline__ uint32_t wait_flag(const ConsumeArgs& a, int64_t f, uint64_t t0, bool* ok) {
+  uint32_t v = __hip_atomic_load(&a.flags[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  bool timed_out = false;
+  while ((int32_t)(v - a.epoch) < 0) {
+    if (wall_clock64() - t0 > a.timeout_ticks) {
+      timed_out = true;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(4);
+    v = __hip_atomic_load(&a.flags[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  *ok = !__builtin_amdgcn_readfirstlane((int)timed_out);
+  if (!*ok && threadIdx.x == 0) {
+    __hip_atomic_store(&a.status[ST_TIMED_OUT], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    atomicMin(&a.status[ST_FIRST_MISSING], (int32_t)f);
+  }
+  return v;
+}
+
+__device__ __forceinline__ u4v load16(__amdgpu_buffer_rsrc_t rs, int off, bool coherent) {
+  return coherent ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16)
+                  : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+}
+
+// Receiver (Sec. III-A, "Book-keeping Flags").  Single-wave workgroups take
+// work items in production order, so the slices that complete last are
+// drained by many waves at once; each item waits for its flag, then copies
+// its data from send to recv.  With coherent_loads the data is read with
+// device-scope loads, which see the producer's device-scope stores without
+// invalidating this XCD's L2; otherwise an agent-scope acquire precedes plain
+// loads.
+//   Whole-slice granule: an item is one 32 KiB piece of a slice's contiguous
+//   C * sum(D) floats.
+//   Per-table granule: an item is one (slice, table) pair: C rows of D_t
+//   floats at columns off_t .. off_t + D_t, row stride sum(D).
 __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
   const int lane = threadIdx.x;
   const uint64_t t0 = wall_clock64();
-  const int64_t n_items = a.so.n_chunks * a.pieces;
+  const int64_t per_slice = a.per_table ? a.T : a.pieces;
+  const int64_t n_items = a.so.n_chunks * per_slice;
   const int64_t chunk_f4 = a.chunk_floats >> 2;
   for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
-    const int64_t gs = x / a.pieces;
-    const int64_t p = x - gs * a.pieces;
+    const int64_t gs = x / per_slice;
+    const int64_t p = x - gs * per_slice;
     const int64_t g = slice_at(a.so, gs);
-    uint32_t v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    bool timed_out = false;
-    while ((int32_t)(v - a.epoch) < 0) {
-      if (wall_clock64() - t0 > a.timeout_ticks) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(4);
-      v = __hip_atomic_load(&a.flags[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    if (__builtin_amdgcn_readfirstlane((int)timed_out)) {
-      if (lane == 0) {
-        __hip_atomic_store(&a.status[ST_TIMED_OUT], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        atomicMin(&a.status[ST_FIRST_MISSING], (int32_t)g);
-      }
-      return;
-    }
-    if (v != a.epoch && p == 0 && lane == 0) atomicAdd(&a.status[ST_OVERSHOOT], 1);
+    const int t = a.per_table ? __builtin_amdgcn_readfirstlane(a.tperm[p]) : 0;
+    const int64_t f = a.per_table ? g * a.T + t : g;
+    bool ok;
+    const uint32_t v = wait_flag(a, f, t0, &ok);
+    if (!ok) return;
+    if (v != a.epoch && (a.per_table || p == 0) && lane == 0) atomicAdd(&a.status[ST_OVERSHOOT], 1);
     if (!a.coherent_loads) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    const int64_t e0 = p * a.piece_f4;
-    const int n = (int)min(a.piece_f4, chunk_f4 - e0);
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.send + g * a.chunk_floats + e0 * 4), 0, n * 16,
-                                          kBufferWord3);
-    float4* dst = reinterpret_cast<float4*>(a.recv + g * a.chunk_floats) + e0;
-    for (int i0 = 0; i0 < n; i0 += 8 * 64) {
-      u4v r[8];
+    if (a.per_table) {
+      // table constants are wave-uniform: keep them (and the descriptor) scalar
+      const int dim = __builtin_amdgcn_readfirstlane(a.meta[t].dim);
+      const int col_off = __builtin_amdgcn_readfirstlane(a.meta[t].col_off);
+      const int v4 = dim >> 2;                         // float4s per row of this table
+      const int64_t base = g * a.chunk_floats + col_off;
+      const int n = a.C * v4;
+      const int ld4 = a.sum_dim >> 2;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<float*>(a.send + base), 0, ((a.C - 1) * a.sum_dim + dim) * 4, kBufferWord3);
+      float4* dst = reinterpret_cast<float4*>(a.recv + base);
+      for (int i0 = 0; i0 < n; i0 += 4 * 64) {
+        u4v r[4];
+        int off[4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * 64 + lane;
-        r[u] = a.coherent_loads ? __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16, 0, 16)
-                                : __builtin_amdgcn_raw_buffer_load_b128(rs, i * 16, 0, 0);
+        for (int u = 0; u < 4; ++u) {
+          const int e = i0 + u * 64 + lane;
+          const int row = e / v4;
+          off[u] = e < n ? row * ld4 + (e - row * v4) : -1;
+          r[u] = load16(rs, off[u] < 0 ? 0 : off[u] * 16, a.coherent_loads);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (off[u] >= 0)
+            dst[off[u]] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
+                                      __uint_as_float(r[u].w));
       }
+    } else {
+      const int64_t e0 = p * a.piece_f4;
+      const int n = (int)min(a.piece_f4, chunk_f4 - e0);
+      const __amdgpu_buffer_rsrc_t rs =
+          __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.send + g * a.chunk_floats + e0 * 4), 0, n * 16,
+                                            kBufferWord3);
+      float4* dst = reinterpret_cast<float4*>(a.recv + g * a.chunk_floats) + e0;
+      for (int i0 = 0; i0 < n; i0 += 8 * 64) {
+        u4v r[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int i = i0 + u * 64 + lane;
-        if (i < n) dst[i] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
-                                        __uint_as_float(r[u].w));
+        for (int u = 0; u < 8; ++u) r[u] = load16(rs, (i0 + u * 64 + lane) * 16, a.coherent_loads);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int i = i0 + u * 64 + lane;
+          if (i < n) dst[i] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
+                                          __uint_as_float(r[u].w));
+        }
       }
     }
-    if (a.trace_drain && lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(&a.trace_drain[g]),
+    if (a.trace_drain && lane == 0) atomicMax(reinterpret_cast<unsigned long long*>(&a.trace_drain[f]),
                                               (unsigned long long)wall_clock64());
   }
 }
@@ -111,7 +155,7 @@ hipError_t launch_repack(const RepackArgs& a, int grid, int block, hipStream_t s
 }
 
 hipError_t launch_publish(const PublishArgs& a, hipStream_t stream) {
-  const int64_t blocks = (a.n_chunks + 255) / 256;
+  const int64_t blocks = (a.n_flags + 255) / 256;
   hipLaunchKernelGGL(publish_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }

@@ -22,7 +22,7 @@ def load(path=PATH):
             elif key == "table":
                 cur = []
                 d["tables"].append(cur)
-            elif key in ("offsets", "indices", "flags"):
+            elif key in ("offsets", "indices", "flags", "flags_per_table"):
                 d[key] = [int(x) for x in rest]
                 cur = None
             elif key == "weights":

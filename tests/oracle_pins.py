@@ -48,6 +48,8 @@ def pin_hand(lib):
     assert np.array_equal(send.reshape(R, S, -1), d["mean"].astype(np.float32)), "hand mean"
     fl = oracle.flags(B, R, C, 1, lib=lib)
     assert fl.tolist() == d["flags"], "hand flags"
+    fl = oracle.flags(B, R, C, 1, lib=lib, per_slice=len(tabs))
+    assert fl.tolist() == d["flags_per_table"], "hand per-table flags"
 
 
 def _random_bags(rng, T, B, rows, max_len, allow_empty=False):

@@ -26,7 +26,10 @@ MUTANTS = {
     "half_sign": ("return sign ? -v : v;", "return v;"),
     "bf16_shift": ("uint32_t bits = (uint32_t)h << 16;", "uint32_t bits = (uint32_t)h << 15;"),
     "no_range_check": ("if (indices[k] < 0 || (int64_t)indices[k] >= rows[t]) return OR_BAD_INDEX;", ""),
-    "flags_off_by_one": ("flags[r * nC + c] = epoch;", "flags[r * nC + c] = epoch + (c == 0);"),
+    "flags_off_by_one": ("flags[(r * nC + c) * per_slice + t] = epoch;",
+                         "flags[(r * nC + c) * per_slice + t] = epoch + (c == 0);"),
+    "flags_per_table_index": ("flags[(r * nC + c) * per_slice + t] = epoch;",
+                              "flags[(r * nC + c) * per_slice + t * 0] = epoch;"),
     "mean_not_divided": ("          sum /= (double)(hi - lo);\n", ""),
     "mean_divides_by_l_plus_one": ("          sum /= (double)(hi - lo);", "          sum /= (double)(hi - lo + 1);"),
     "round_down": ("if (J->send) J->send[out + j] = (float)sum;", "if (J->send) J->send[out + j] = (float)floor(sum);"),
