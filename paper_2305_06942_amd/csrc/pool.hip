@@ -2,19 +2,26 @@
 //
 // One wavefront pools one bag at a time (the paper's "logical workgroup" of
 // the EmbeddingBag kernel, Sec. III-A).  A workgroup takes a *run* of up to K
-// consecutive samples of one table inside one slice, its waves share the
-// run's bags, and after the run the workgroup bumps that slice's counter
-// once; the arrival that completes the slice releases the slice's flag
-// (Sec. III-A, "Book-keeping Flags" / "Synchronization").
+// consecutive samples of one table inside one slice and its waves share the
+// run's bags; after the run the workgroup bumps that slice's counter once,
+// and the arrival that completes the slice releases the slice's flag
+// (Sec. III-A, "Book-keeping Flags").
 //
 // Gather: a row of D_t elements is V = D_t*elt/16 sixteen-byte vectors.  For
 // V a power of two <= 64 the 64 lanes form G = 64/V row groups, lane (g, v)
 // loads vector v of rows g, g+G, g+2G, ... so one wave instruction fetches G
 // whole rows (1 KiB) with fully coalesced 16-byte loads; every wave keeps U
-// such loads in flight.  The bag's index run is first staged in LDS with
-// coalesced loads and then read back by broadcast.  Partial sums of the G
-// groups are combined with cross-lane xor-shuffles and lanes of group 0 store
-// the fp32 result straight to its destination slot.
+// such loads in flight.  A wave's block of bags has its index run staged in
+// LDS with coalesced loads and read back by broadcast.  Partial sums of the G
+// groups are combined with cross-lane xor-shuffles.
+//
+// Fast path (tables < 4 GiB, V = 2^k, no index checks): each pooled row goes
+// to an LDS tile of the run; the last wave of the workgroup to finish writes
+// the whole run to its destination slots with contiguous 16-byte stores,
+// waits for them and updates the slice counter -- no workgroup barrier, and
+// no store queued ahead of a gather load.  General path (any width, index
+// checks): per-bag staging, rows stored directly, a barrier before the
+// counter update.
 //
 // Run order: runs are numbered slice-major (all runs of slice 0, then slice 1
 // ...), tables fastest inside a slice, so slices complete progressively and a
@@ -415,10 +422,11 @@ constexpr int SEGW = 512;  // indices a wave stages at once for a block of bags
 
 // One workgroup per run: up to K consecutive samples of one table inside one
 // slice.  The counter it feeds is the slice's (target C * T bags) or, with
-// per-table slices, the (slice, table) pair's (target C bags).  Wave w pools a contiguous block of the run's bags: it loads the
-// block's CSR offsets with one vector load, stages the block's whole index
-// segment into its LDS slot when it fits (else bag by bag, SEG at a time),
-// then gathers, reduces and stores every bag.
+// per-table slices, the (slice, table) pair's (target C bags).  On the fast
+// path wave w pools a contiguous block of the run's bags: it reads the
+// block's CSR offsets with scalar loads, stages the block's whole index
+// segment into its LDS slot when it fits (else bag by bag, SEGW at a time),
+// then gathers and reduces every bag into the run's LDS tile.
 template <class E, int U, bool WT, bool FUSED, bool SAFE>
 __device__ __forceinline__ void pool_body(const PoolArgs& a) {
   constexpr int EPV = E::EPV;
