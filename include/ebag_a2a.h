@@ -90,7 +90,9 @@ typedef struct ebag_a2a_opts {
   int32_t waves_per_wg;        /* wavefronts (64 lanes) per pooling workgroup, 1..16 (default 4) */
   int32_t bags_per_run;        /* bags a workgroup pools before one slice-counter update (default 16) */
   int32_t rows_in_flight;      /* 16-byte row loads each wave keeps in flight: 4, 8 or 16 (default 8) */
-  int32_t persistent_wgs_per_cu; /* 0: one workgroup per run; >0: persistent grid of that many WGs per CU */
+  int32_t persistent_wgs_per_cu; /* 0: one workgroup per run; >0: persistent grid of that many WGs per CU
+                                    (-1: as many as fit), whose workgroups claim runs in production order
+                                    from an atomic ticket (Sec. III-A task loop) */
   int32_t release_mode;        /* slice release: 1 (default) device-scope stores + completion wait, 0 agent-scope release fence per run */
   int32_t chunk_order;         /* 0: natural slice order; 1: slices of destination self_rank last */
   int32_t self_rank;           /* the destination whose slices stay local (chunk_order == 1) */
@@ -186,8 +188,8 @@ int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_fla
  */
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]);
 
-/* Zero the slice counters and the status word (after a timeout or an
- * aborted sequence).  Synchronous. */
+/* Zero the slice counters, the persistent-grid ticket and the status word
+ * (after a timeout or an aborted sequence).  Synchronous. */
 int ebag_a2a_reset(ebag_a2a_t h);
 
 /*

@@ -49,6 +49,7 @@ struct PoolArgs {
   uint32_t* flags;            // [n_flags] epoch flags
   int32_t* status;            // plan status word
   uint64_t* trace_release;    // [n_flags] or nullptr
+  uint32_t* ticket;           // [2] persistent grid: next run, workgroups done (self-resetting)
   int64_t B;
   int64_t nruns;
   int64_t suppress;           // flag index never released (-1: none)

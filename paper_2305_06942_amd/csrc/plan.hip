@@ -129,6 +129,7 @@ struct ebag_a2a_plan {
   uint32_t* d_counters = nullptr;
   float* d_scratch = nullptr;
   int32_t* d_status = nullptr;
+  uint32_t* d_ticket = nullptr;  // persistent-grid run ticket [2], self-resetting
   uint64_t* d_trace_release = nullptr;
   uint64_t* d_trace_drain = nullptr;
 };
@@ -145,6 +146,7 @@ void free_plan(ebag_a2a_plan* h) {
   (void)hipFree(h->d_counters);
   (void)hipFree(h->d_scratch);
   (void)hipFree(h->d_status);
+  (void)hipFree(h->d_ticket);
   (void)hipFree(h->d_trace_release);
   (void)hipFree(h->d_trace_drain);
   delete h;
@@ -231,6 +233,7 @@ void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_
   a->flags = flags;
   a->status = h->d_status;
   a->trace_release = h->opts.trace ? h->d_trace_release : nullptr;
+  a->ticket = h->d_ticket;
   a->B = B;
   a->K = K;
   a->J = (h->C + K - 1) / K;
@@ -380,6 +383,8 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   CREATE_TRY(hipMalloc((void**)&h->d_counters, sizeof(uint32_t) * h->max_flags), "alloc slice counters");
   CREATE_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero slice counters");
   CREATE_TRY(hipMalloc((void**)&h->d_scratch, sizeof(float) * (size_t)max_batch * (size_t)sum_dim), "alloc scratch");
+  CREATE_TRY(hipMalloc((void**)&h->d_ticket, 2 * sizeof(uint32_t)), "alloc run ticket");
+  CREATE_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
   CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
   CREATE_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "init status");
   if (o.trace) {
@@ -405,6 +410,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, send_buf, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
+  if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
   const int grid = pool_grid(h, a.nruns, true, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(h), a, grid,
                              block, stream);
@@ -423,6 +429,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   PoolArgs a;
   fill_pool_args(h, indices, offsets, weights, B, so, h->d_scratch, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
+  if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
   const int grid = pool_grid(h, a.nruns, false, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(h), a, grid,
                              block, stream);
@@ -519,6 +526,7 @@ int ebag_a2a_reset(ebag_a2a_t h) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero counters");
+  HIP_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
   HIP_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "reset status");
   if (h->d_trace_release) {
     HIP_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_flags), "zero trace");

@@ -420,6 +420,29 @@ __device__ __forceinline__ void wait_stores_complete() { __builtin_amdgcn_s_wait
 
 constexpr int SEGW = 512;  // indices a wave stages at once for a block of bags
 
+// Persistent grid: workgroups claim runs in production order from an atomic
+// ticket (ticket[0]).  The leading barrier makes sure every wave is done with
+// the previous run (its LDS tile and the broadcast slot) before the slot is
+// rewritten.
+__device__ __forceinline__ int64_t draw_run(uint32_t* ticket, uint32_t* s_tick) {
+  __syncthreads();
+  if (threadIdx.x == 0) *s_tick = __hip_atomic_fetch_add(&ticket[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  return (int64_t)__builtin_amdgcn_readfirstlane(*s_tick);
+}
+
+// A workgroup whose draw came back past the last run counts itself out in
+// ticket[1]; the last one re-arms both words for the next launch.  Every
+// workgroup's final draw has returned (its value decided the exit) before it
+// counts itself out, so no draw of this launch can follow the re-arm.
+__device__ __forceinline__ void leave_runs(uint32_t* ticket) {
+  if (threadIdx.x == 0 &&
+      __hip_atomic_fetch_add(&ticket[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gridDim.x - 1) {
+    __hip_atomic_store(&ticket[0], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&ticket[1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
 // One workgroup per run: up to K consecutive samples of one table inside one
 // slice.  The counter it feeds is the slice's (target C * T bags) or, with
 // per-table slices, the (slice, table) pair's (target C bags).  On the fast
@@ -448,7 +471,12 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
   const bool sc1 = FUSED && a.release_mode == 1;
   const int64_t per_slice = (int64_t)a.T * a.J;
   const int64_t nnz = (!SAFE || a.check) ? sload(a.offsets, (int64_t)a.T * a.B) : 0;
-  for (int64_t q = blockIdx.x; q < a.nruns; q += gridDim.x) {
+  // One-shot grid: workgroup i pools run i.  Persistent grid (fewer
+  // workgroups than runs): runs are claimed from the ticket.
+  const bool persistent = gridDim.x < a.nruns;
+  uint32_t* s_tick = SAFE ? reinterpret_cast<uint32_t*>(lds_out) : reinterpret_cast<uint32_t*>(s_arrive + 1);
+  for (int64_t q = persistent ? draw_run(a.ticket, s_tick) : (int64_t)blockIdx.x; q < a.nruns;
+       q = persistent ? draw_run(a.ticket, s_tick) : a.nruns) {
     const int64_t gs = q / per_slice;
     const int64_t rem = q - gs * per_slice;
     const int tpos = (int)(rem % a.T);
@@ -540,8 +568,6 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
                           a.release_mode);
         }
       }
-      // A persistent workgroup reuses the LDS output buffer for its next run.
-      if (gridDim.x < a.nruns) __syncthreads();
     } else {
       for (int64_t b = bb; b < be; ++b) {
         int64_t lo = a.offsets[obase + b];
@@ -585,6 +611,7 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
                       a.release_mode);
     }
   }
+  if (persistent) leave_runs(a.ticket);
 }
 
 // Fused operator: pooled vectors go straight to the send layout and slices
@@ -631,8 +658,9 @@ pool_fn pick(int dtype, int u, bool weighted, bool fused, bool safe) {
 }
 
 size_t lds_bytes(bool safe, bool weighted, int block, int out_floats) {
+  // + 16 bytes: the run-arrival counter and the ticket broadcast slot
   const size_t staging = (size_t)(block / 64) * (safe ? SEG : SEGW) * (weighted ? 8 : 4);
-  return safe ? staging : staging + (size_t)out_floats * 4 + 16;
+  return safe ? staging + 16 : staging + (size_t)out_floats * 4 + 16;
 }
 
 }  // namespace

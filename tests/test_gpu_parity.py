@@ -163,26 +163,35 @@ def test_edge_cases(name):
 
 @pytest.mark.parametrize("name", ["tiny", "dlrm", "skewed", "mixed", "large"])
 def test_full_size_sampled(name):
-    """Full workload sizes: sampled bags element by element against the
-    oracle, every flag equal to the epoch, fused and unfused."""
+    """Full workload sizes, in the launch configuration the benchmark times
+    (and in the default one where they differ): sampled bags element by
+    element against the oracle, every element written, every flag equal to
+    the epoch, fused and unfused."""
     import torch
+    import bench
     w = synth.FULL[name]
     say("full", name, "generating inputs")
     inp = synth.make_inputs(w)
     say("full", name, "nnz", inp.nnz, "to device")
     dev = sdev.to_device(inp)
-    plan = make_plan(w)
+    configs = [dict(bench.PLAN_OPTS.get(name, {}))]
+    if configs[0]:
+        configs.append({})
     send, _, flags = new_buffers(w)
-    for fused in (True, False):
-        flags.zero_()
-        send.fill_(float("nan"))
-        run(plan, w, dev, send, flags, fused=fused)
-        torch.cuda.synchronize()
-        say("full", name, "fused" if fused else "unfused", "ran; checking")
-        assert not torch.isnan(send).any().item(), "some output element was never written"
-        assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
-        n = check_sampled(inp, send, n_bags=200)
-        say("full", name, "checked", n, "bags")
+    for opts in configs:
+        plan = make_plan(w, **opts)
+        for fused in (True, False):
+            flags.zero_()
+            send.fill_(float("nan"))
+            run(plan, w, dev, send, flags, fused=fused)
+            torch.cuda.synchronize()
+            say("full", name, opts, "fused" if fused else "unfused", "ran; checking")
+            assert not torch.isnan(send).any().item(), "some output element was never written"
+            assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+            n = check_sampled(inp, send, n_bags=200)
+            say("full", name, "checked", n, "bags")
+        assert plan.status_ex() == (0, -1, 0, -1)
+        plan.close()
     del dev, send, flags
     torch.cuda.empty_cache()
 
@@ -224,3 +233,27 @@ def test_gather_probe_reads_in_bounds_rows():
         torch.cuda.synchronize()
         assert n == grid * 4 * 16 * 1024
         assert int(out.abs().sum()) == 0
+
+
+@pytest.mark.parametrize("per_cu", [1, 3, -1])
+def test_persistent_ticket_rearms_every_launch(per_cu):
+    """Persistent grids claim runs from a ticket that the last workgroup out
+    re-arms: several launches in a row (fused and unfused, both granules)
+    each pool every bag and publish every flag once."""
+    import torch
+    w = SMALL["skewed_small"]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    for granule in (0, 1):
+        plan = make_plan(w, persistent_wgs_per_cu=per_cu, slice_granule=granule, bags_per_run=4)
+        per_slice = w.T if granule else 1
+        send, _, _ = new_buffers(w)
+        flags = torch.zeros(w.n_chunks * per_slice, dtype=torch.int32, device="cuda")
+        for epoch in range(1, 5):
+            send.fill_(float("nan"))
+            run(plan, w, dev, send, flags, fused=epoch % 2 == 1)
+            torch.cuda.synchronize()
+            check_full(inp, send.cpu().numpy(), s64, a64)
+            assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, epoch, per_slice=per_slice))
+        assert plan.status_ex() == (0, -1, 0, -1)
