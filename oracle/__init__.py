@@ -5,7 +5,10 @@ and by the benchmark's CPU-baseline leg, never by the product package.  It
 shares no code with the GPU path; the only thing both sides use is the seeded
 input generator in ``synth``.
 
-Three implementations of the same definition (pooled sums in fp64, placed at
+GEMV + AllReduce (Sec. III-B): :func:`gemv_ar` computes the reduced vector
+every rank holds after the AllReduce, sum over ranks of A_r x_r, in fp64.
+
+Three implementations of the same pooling definition (pooled sums in fp64, placed at
 send[r][s][off_t + j] with r = b / S, s = b mod S; one flag per
 (destination, slice) equal to the epoch), each usable as a check of the others:
 
@@ -55,6 +58,8 @@ def load(path: str = LIB):
     lib.oracle_validate.restype = ctypes.c_int
     lib.oracle_flags.argtypes = [i64, i32, i32, i32, ctypes.c_uint32, P, i64]
     lib.oracle_flags.restype = ctypes.c_int
+    lib.oracle_gemv_ar.argtypes = [i32, i64, P, i32, P, P, P, P, P, i32]
+    lib.oracle_gemv_ar.restype = ctypes.c_int
     lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
     lib.oracle_half_to_double.restype = ctypes.c_double
     lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
@@ -124,6 +129,37 @@ def flags(B, R, C, epoch, lib=None, per_slice=1):
     if rc != 0:
         raise OracleError(f"oracle_flags: {ERRORS.get(rc, rc)}")
     return out
+
+
+def gemv_ar(A, x, dtype, nthreads=None, lib=None):
+    """GEMV + AllReduce (Sec. III-B): A and x are lists of R host arrays in
+    storage dtype, A[r] of shape (M, K_r), x[r] of K_r elements.  Returns
+    (y64, abs64, y) -- the sum over ranks of A_r x_r in fp64, the sum of
+    |terms|, and the fp32 result every rank holds after the AllReduce."""
+    lib = lib or load()
+    R = len(A)
+    if R == 0 or len(x) != R:
+        raise OracleError("bad arguments")
+    As = [np.ascontiguousarray(a) for a in A]
+    xs = [np.ascontiguousarray(v) for v in x]
+    M = As[0].shape[0]
+    for a, v in zip(As, xs):
+        if a.ndim != 2 or a.shape[0] != M or v.shape != (a.shape[1],):
+            raise OracleError("bad arguments")
+    Ks = np.array([a.shape[1] for a in As], dtype=np.int64)
+    pa = (ctypes.c_void_p * R)(*[a.ctypes.data for a in As])
+    px = (ctypes.c_void_p * R)(*[v.ctypes.data for v in xs])
+    y64 = np.empty(M, dtype=np.float64)
+    abs64 = np.empty(M, dtype=np.float64)
+    y = np.empty(M, dtype=np.float32)
+    if nthreads is None:
+        nthreads = len(os.sched_getaffinity(0))
+    rc = lib.oracle_gemv_ar(R, M, Ks.ctypes.data, dtype, ctypes.cast(pa, ctypes.c_void_p),
+                            ctypes.cast(px, ctypes.c_void_p), y64.ctypes.data, abs64.ctypes.data, y.ctypes.data,
+                            nthreads)
+    if rc != 0:
+        raise OracleError(f"oracle_gemv_ar: {ERRORS.get(rc, rc)}")
+    return y64, abs64, y
 
 
 def within_tolerance(gpu, sum64, abs64, rel=1e-5, absol=1e-6):

@@ -1,5 +1,6 @@
 /*
- * CPU oracle for the fused embedding-pooling + All-to-All send layout.
+ * CPU oracle for the fused embedding-pooling + All-to-All send layout, and
+ * for the GEMV + AllReduce operator (at the end of this file).
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
  * calls this file; only the tests, the smoke check and the benchmark's CPU
@@ -207,5 +208,74 @@ int oracle_flags(int64_t B, int32_t R, int32_t C, int32_t per_slice, uint32_t ep
   for (int64_t r = 0; r < R; ++r)
     for (int64_t c = 0; c < nC; ++c)
       for (int32_t t = 0; t < per_slice; ++t) flags[(r * nC + c) * per_slice + t] = epoch;
+  return OR_OK;
+}
+
+/*
+ * GEMV + AllReduce (Sec. III-B, scale-up operator): R ranks; rank r holds a
+ * row-major M x K_r matrix A_r and a vector x_r of K_r elements (the
+ * column split of y = A x in a tensor-parallel layer).  The AllReduce leaves
+ * on every rank y = sum over r of A_r x_r, M elements.
+ *   A, x   : R host pointers each, storage dtype (fp32 / fp16 / bf16)
+ *   Ks     : K_r per rank (> 0)
+ *   y64, abs64 : [M] fp64 sum and sum of |terms| (either may be NULL)
+ *   y      : [M] fp32, the fp64 sum rounded to nearest-even (may be NULL)
+ * Terms are accumulated in fp64, rank by rank, then column by column.
+ */
+typedef struct {
+  int32_t R;
+  int64_t M;
+  const int64_t* Ks;
+  int32_t dtype;
+  const void* const* A;
+  const void* const* x;
+  double* y64;
+  double* abs64;
+  float* y;
+  int64_t i_begin, i_end;
+} gemv_job_t;
+
+static void* gemv_rows(void* arg) {
+  const gemv_job_t* J = (const gemv_job_t*)arg;
+  for (int64_t i = J->i_begin; i < J->i_end; ++i) {
+    double sum = 0.0, mag = 0.0;
+    for (int32_t r = 0; r < J->R; ++r) {
+      const int64_t K = J->Ks[r];
+      for (int64_t k = 0; k < K; ++k) {
+        const double term = load_elem(J->A[r], J->dtype, i * K + k) * load_elem(J->x[r], J->dtype, k);
+        sum = sum + term;
+        mag = mag + fabs(term);
+      }
+    }
+    if (J->y64) J->y64[i] = sum;
+    if (J->abs64) J->abs64[i] = mag;
+    if (J->y) J->y[i] = (float)sum;
+  }
+  return NULL;
+}
+
+int oracle_gemv_ar(int32_t R, int64_t M, const int64_t* Ks, int32_t dtype, const void* const* A,
+                   const void* const* x, double* y64, double* abs64, float* y, int32_t nthreads) {
+  if (R <= 0 || M <= 0 || !Ks || !A || !x || dtype < OR_F32 || dtype > OR_BF16) return OR_BAD_ARGS;
+  for (int32_t r = 0; r < R; ++r)
+    if (Ks[r] <= 0 || !A[r] || !x[r]) return OR_BAD_ARGS;
+  if (nthreads <= 0) nthreads = 1;
+  if (nthreads > M) nthreads = (int32_t)M;
+  gemv_job_t* jobs = (gemv_job_t*)calloc((size_t)nthreads, sizeof(gemv_job_t));
+  pthread_t* th = (pthread_t*)calloc((size_t)nthreads, sizeof(pthread_t));
+  if (!jobs || !th) {
+    free(jobs);
+    free(th);
+    return OR_BAD_ARGS;
+  }
+  for (int32_t t = 0; t < nthreads; ++t) {
+    gemv_job_t J = {R, M, Ks, dtype, A, x, y64, abs64, y, M * t / nthreads, M * (t + 1) / nthreads};
+    jobs[t] = J;
+  }
+  for (int32_t t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, gemv_rows, &jobs[t]);
+  gemv_rows(&jobs[0]);
+  for (int32_t t = 1; t < nthreads; ++t) pthread_join(th[t], NULL);
+  free(th);
+  free(jobs);
   return OR_OK;
 }

@@ -43,3 +43,30 @@ def load(path=PATH):
             arr[r, s] = v
         d[k] = arr
     return d
+
+
+GEMV_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "gemv_hand.txt")
+
+
+def load_gemv(path=GEMV_PATH):
+    """Parse the hand-worked GEMV + AllReduce fixture: per-rank A rows and x,
+    and the expected y and sum of |terms|."""
+    A, x = {}, {}
+    d = {}
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, *rest = line.split()
+            vals = [float(v) for v in rest]
+            if key.startswith("A"):
+                A.setdefault(int(key[1:]), []).append(vals)
+            elif key.startswith("x"):
+                x[int(key[1:])] = vals
+            else:
+                d[key] = np.array(vals)
+    R = len(A)
+    d["A"] = [np.array(A[r]) for r in range(R)]
+    d["x"] = [np.array(x[r]) for r in range(R)]
+    return d

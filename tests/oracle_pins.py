@@ -337,6 +337,84 @@ def pin_validation(lib):
         raise AssertionError("mean pooling with weights accepted")
 
 
+# ---- GEMV + AllReduce (Sec. III-B) -----------------------------------------
+
+
+def pin_gemv_hand(lib):
+    d = hand.load_gemv()
+    A = [a.astype(np.float32) for a in d["A"]]
+    x = [v.astype(np.float32) for v in d["x"]]
+    y64, abs64, y = oracle.gemv_ar(A, x, 0, nthreads=2, lib=lib)
+    assert np.array_equal(y64, d["y"]) and np.array_equal(abs64, d["abs"]), (y64, abs64)
+    assert np.array_equal(y, d["y"].astype(np.float32))
+
+
+def pin_gemv_integer_exact(lib):
+    """Integer matrices and vectors: exact, compared with Python integers, for
+    every storage type."""
+    rng = np.random.default_rng(31)
+    R, M = 3, 37
+    Ks = [5, 64, 17]
+    for dtype in (0, 1, 2):
+        ia = [rng.integers(-8, 9, size=(M, K)) for K in Ks]
+        ix = [rng.integers(-8, 9, size=K) for K in Ks]
+
+        def enc(v):
+            if dtype == 0:
+                return v.astype(np.float32)
+            if dtype == 1:
+                return v.astype(np.float16)
+            return (v.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        y64, abs64, y = oracle.gemv_ar([enc(a) for a in ia], [enc(v) for v in ix], dtype, nthreads=2, lib=lib)
+        for i in range(M):
+            terms = [int(ia[r][i, k]) * int(ix[r][k]) for r in range(R) for k in range(Ks[r])]
+            assert y64[i] == float(sum(terms)) and abs64[i] == float(sum(abs(t) for t in terms)), (dtype, i)
+            assert y[i] == np.float32(sum(terms))
+
+
+def pin_gemv_matmul(lib):
+    """Special case that reduces to a library routine: the column blocks
+    concatenate to A = [A_0 | ... | A_{R-1}], x to their stacked parts, and the
+    result is numpy's fp64 A @ x."""
+    rng = np.random.default_rng(37)
+    Ks = [40, 7, 128, 33]
+    M = 90
+    A = [rng.standard_normal((M, K)).astype(np.float32) for K in Ks]
+    x = [rng.standard_normal(K).astype(np.float32) for K in Ks]
+    y64, abs64, y = oracle.gemv_ar(A, x, 0, nthreads=3, lib=lib)
+    full = np.concatenate([a.astype(np.float64) for a in A], axis=1)
+    xv = np.concatenate([v.astype(np.float64) for v in x])
+    assert np.allclose(y64, full @ xv, rtol=1e-12, atol=1e-12)
+    assert np.allclose(abs64, np.abs(full) @ np.abs(xv), rtol=1e-12, atol=1e-12)
+    assert np.all(np.abs(y.astype(np.float64) - y64) <= 2.0 ** -24 * np.abs(y64) + 1e-300)
+
+
+def pin_gemv_closed_forms(lib):
+    """All-ones matrices give the sum of every rank's x in each row; an
+    identity block on rank 0 with zero blocks elsewhere returns x_0."""
+    rng = np.random.default_rng(41)
+    Ks = [6, 10]
+    M = 6
+    x = [rng.integers(-100, 100, size=K).astype(np.float32) for K in Ks]
+    y64, _, _ = oracle.gemv_ar([np.ones((M, K), np.float32) for K in Ks], x, 0, nthreads=1, lib=lib)
+    assert np.all(y64 == float(sum(v.astype(np.int64).sum() for v in x)))
+    A = [np.eye(M, Ks[0], dtype=np.float32), np.zeros((M, Ks[1]), np.float32)]
+    y64, _, y = oracle.gemv_ar(A, x, 0, nthreads=1, lib=lib)
+    assert np.array_equal(y, x[0])
+
+
+def pin_gemv_validation(lib):
+    A = [np.zeros((4, 3), np.float32)]
+    for bad in ([np.zeros(4, np.float32)], [np.zeros(3, np.float32), np.zeros(3, np.float32)]):
+        try:
+            oracle.gemv_ar(A, bad, 0, lib=lib)
+        except oracle.OracleError:
+            pass
+        else:
+            raise AssertionError("shape mismatch accepted")
+
+
 ALL_PINS = [pin_hand, pin_integer_exact, pin_ones_and_weights, pin_row_coded, pin_placement,
             pin_fp16_decode, pin_bf16_decode, pin_fp16_pool, pin_torch_embedding_bag, pin_mean_closed_forms,
-            pin_torch_embedding_bag_mean, pin_validation]
+            pin_torch_embedding_bag_mean, pin_validation, pin_gemv_hand, pin_gemv_integer_exact, pin_gemv_matmul,
+            pin_gemv_closed_forms, pin_gemv_validation]

@@ -32,6 +32,11 @@ MUTANTS = {
                               "flags[(r * nC + c) * per_slice + t * 0] = epoch;"),
     "mean_not_divided": ("          sum /= (double)(hi - lo);\n", ""),
     "mean_divides_by_l_plus_one": ("          sum /= (double)(hi - lo);", "          sum /= (double)(hi - lo + 1);"),
+    "gemv_drop_rank": ("for (int32_t r = 0; r < J->R; ++r) {", "for (int32_t r = 0; r + 1 < J->R; ++r) {"),
+    "gemv_transposed": ("load_elem(J->A[r], J->dtype, i * K + k)", "load_elem(J->A[r], J->dtype, k * J->M + i)"),
+    "gemv_x_reversed": ("load_elem(J->x[r], J->dtype, k)", "load_elem(J->x[r], J->dtype, K - 1 - k)"),
+    "gemv_abs_not_abs": ("mag = mag + fabs(term);", "mag = mag + term;"),
+    "gemv_no_rounding_to_f32": ("if (J->y) J->y[i] = (float)sum;", "if (J->y) J->y[i] = (float)(sum + 1e-3);"),
     "round_down": ("if (J->send) J->send[out + j] = (float)sum;", "if (J->send) J->send[out + j] = (float)floor(sum);"),
 }
 
