@@ -1,9 +1,10 @@
-"""Fused embedding-bag pooling + All-to-All send layout for MI355X (gfx950).
+"""Fused embedding-bag pooling + All-to-All send layout, and fused GEMV +
+AllReduce, for MI355X (gfx950).
 
 Python binding of the C ABI in ``include/ebag_a2a.h`` (argument marshalling
 only: every step of the operation runs in the HIP library
 ``libebag_a2a.so`` built next to this file).  There is no fallback: if the
 library is missing, :func:`load` raises.
 """
-from .abi import (EBAG_BF16, EBAG_F16, EBAG_F32, EbagError, Plan, default_opts, last_error,  # noqa: F401
-                  load, queue_stream, symbols)
+from .abi import (EBAG_BF16, EBAG_F16, EBAG_F32, EbagError, GemvAR, Plan, default_opts,  # noqa: F401
+                  gemv_default_opts, last_error, load, queue_stream, symbols)

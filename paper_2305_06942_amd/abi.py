@@ -1,4 +1,5 @@
-"""ctypes binding of include/ebag_a2a.h (same names, argument marshalling only).
+"""ctypes binding of include/ebag_a2a.h and include/gemv_ar.h (same names,
+argument marshalling only).
 
 Device buffers may be passed as torch tensors (their ``data_ptr()`` is used)
 or as integer device addresses.  The stream defaults to torch's current
@@ -37,6 +38,18 @@ class Opts(ctypes.Structure):
     ]
 
 
+class GemvOpts(ctypes.Structure):
+    _fields_ = [
+        ("tile_rows", ctypes.c_int32),
+        ("wgs_per_rank", ctypes.c_int32),
+        ("waves_per_wg", ctypes.c_int32),
+        ("comm_aware", ctypes.c_int32),
+        ("debug_suppress_flag", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("timeout_us", ctypes.c_int64),
+    ]
+
+
 class EbagError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"ebag_a2a error {code}: {msg}")
@@ -61,6 +74,14 @@ _SIGS = {
     "ebag_a2a_queue_stream_create": ([_P], ctypes.c_int),
     "ebag_a2a_destroy": ([_P], None),
     "ebag_a2a_last_error": ([], ctypes.c_char_p),
+    "gemv_ar_default_opts": ([_P], ctypes.c_int),
+    "gemv_ar_create": ([_P, ctypes.c_int32, ctypes.c_int64, _P, ctypes.c_int, _P], ctypes.c_int),
+    "gemv_ar_forward": ([_P, _P, _P, _P, _P, _P], ctypes.c_int),
+    "gemv_ar_unfused_forward": ([_P, _P, _P, _P, _P, _P], ctypes.c_int),
+    "gemv_ar_status": ([_P, _P], ctypes.c_int),
+    "gemv_ar_reset": ([_P], ctypes.c_int),
+    "gemv_ar_launch_info": ([_P, _P], ctypes.c_int),
+    "gemv_ar_destroy": ([_P], None),
 }
 
 
@@ -206,6 +227,74 @@ class Plan:
     def close(self):
         if getattr(self, "_h", None):
             self._lib.ebag_a2a_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def gemv_default_opts() -> GemvOpts:
+    o = GemvOpts()
+    _check(load().gemv_ar_default_opts(ctypes.byref(o)))
+    return o
+
+
+class GemvAR:
+    """A fused GEMV + AllReduce plan (``gemv_ar_create``) for R ranks; methods
+    mirror the C ABI.  A, x, y are sequences of R device buffers."""
+
+    def __init__(self, R: int, M: int, K: Sequence[int], dtype: int, **opts):
+        lib = load()
+        o = gemv_default_opts()
+        for k, v in opts.items():
+            if not hasattr(o, k):
+                raise TypeError(f"unknown option {k}")
+            setattr(o, k, int(v))
+        self.R, self.M, self.K = int(R), int(M), [int(k) for k in K]
+        self.opts = o
+        ks = (ctypes.c_int64 * len(self.K))(*self.K)
+        h = ctypes.c_void_p()
+        _check(lib.gemv_ar_create(ctypes.byref(h), self.R, self.M, ks, int(dtype), ctypes.byref(o)))
+        self._h = h
+        self._lib = lib
+
+    def _arrays(self, A, x, y):
+        if not (len(A) == len(x) == len(y) == self.R):
+            raise ValueError(f"expected {self.R} buffers each for A, x and y")
+        arr = ctypes.c_void_p * self.R
+        return arr(*[_addr(a) for a in A]), arr(*[_addr(v) for v in x]), arr(*[_addr(v) for v in y])
+
+    def forward(self, A, x, y, out_flags=None, stream=None):
+        a, xv, yv = self._arrays(A, x, y)
+        _check(self._lib.gemv_ar_forward(self._h, a, xv, yv, _addr(out_flags), _stream(stream)))
+
+    def unfused_forward(self, A, x, y, out_flags=None, stream=None):
+        a, xv, yv = self._arrays(A, x, y)
+        _check(self._lib.gemv_ar_unfused_forward(self._h, a, xv, yv, _addr(out_flags), _stream(stream)))
+
+    def status(self):
+        """(timed_out, first missing peer flag); synchronises the device."""
+        s = (ctypes.c_int32 * 2)()
+        rc = self._lib.gemv_ar_status(self._h, s)
+        if rc not in (EBAG_OK, EBAG_ETIMEOUT):
+            _check(rc)
+        return s[0], s[1]
+
+    def reset(self):
+        _check(self._lib.gemv_ar_reset(self._h))
+
+    def launch_info(self):
+        """(workgroups per rank P, threads per workgroup, tiles, resident workgroups)."""
+        s = (ctypes.c_int32 * 4)()
+        _check(self._lib.gemv_ar_launch_info(self._h, s))
+        return tuple(s)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.gemv_ar_destroy(self._h)
             self._h = None
 
     def __del__(self):

@@ -113,6 +113,10 @@ struct ConsumeArgs {
 // Status word layout (int32[4]).
 enum { ST_TIMED_OUT = 0, ST_FIRST_MISSING = 1, ST_OVERSHOOT = 2, ST_FIRST_BAD_BAG = 3 };
 
+// Error reporting shared by every entry point (thread-local message).
+int fail(int code, const char* fmt, ...);
+void clear_error();
+
 // Launchers (return hipError_t of the launch).
 hipError_t launch_pool(int dtype, int rows_in_flight, bool weighted, bool fused, bool safe, const PoolArgs& a,
                        int grid, int block, hipStream_t stream);

@@ -18,7 +18,11 @@ namespace {
 
 thread_local std::string g_err;
 
-int fail(int code, const char* fmt, ...) {
+}  // namespace
+
+// Record the calling thread's error message (shared by every entry point of
+// the library, read back with ebag_a2a_last_error).
+int ebag::fail(int code, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -27,6 +31,10 @@ int fail(int code, const char* fmt, ...) {
   g_err = buf;
   return code;
 }
+
+void ebag::clear_error() { g_err.clear(); }
+
+namespace {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(EBAG_EHIP, "%s: %s", what, hipGetErrorString(e));
@@ -565,7 +573,7 @@ int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]) {
   out[1] = h->num_cus;
   out[2] = block;
   out[3] = a.K;
-  g_err.clear();
+  clear_error();
   return EBAG_OK;
 }
 

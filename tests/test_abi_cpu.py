@@ -7,13 +7,19 @@ import re
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "ebag_a2a.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("ebag_a2a.h", "gemv_ar.h")]
 
 
 def _declared():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(ebag_a2a_\w+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b((?:ebag_a2a|gemv_ar)_\w+)\s*\(", src))
+    return sorted(names)
+
+
+def test_every_header_is_checked():
+    assert sorted(os.listdir(os.path.join(ROOT, "include"))) == sorted(os.path.basename(h) for h in HEADERS)
 
 
 @pytest.fixture(scope="module")
@@ -25,7 +31,7 @@ def lib():
 def test_exports_every_declared_symbol(lib):
     import paper_2305_06942_amd as ebag
     names = _declared()
-    assert len(names) >= 10
+    assert len(names) >= 18
     for n in names:
         assert hasattr(lib, n), f"{n} declared in the header but not exported"
     assert set(names) == set(ebag.symbols()), "binding and header disagree"
@@ -93,3 +99,29 @@ def test_package_has_no_fallback():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 src = open(os.path.join(dp, f)).read()
                 assert "oracle" not in src.replace("Oracle", ""), f
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(R=0), "R="), (dict(R=17), "R="), (dict(M=0), "M="), (dict(K=(8, 0)), "K[1]"),
+    (dict(K=(8, 6)), "multiple of 16"), (dict(dtype=5), "dtype"), (dict(K=(8, 1 << 20)), "LDS"),
+])
+def test_gemv_create_rejects(lib, kw, msg):
+    import paper_2305_06942_amd as ebag
+    args = dict(R=2, M=100, K=(8, 8), dtype=0)
+    args.update(kw)
+    K = args["K"] if len(args["K"]) >= max(args["R"], 1) else tuple(args["K"]) * args["R"]
+    h = ctypes.c_void_p()
+    ks = (ctypes.c_int64 * len(K))(*K)
+    rc = lib.gemv_ar_create(ctypes.byref(h), args["R"], args["M"], ks, args["dtype"], None)
+    assert rc in (ebag.abi.EBAG_EINVAL, ebag.abi.EBAG_EUNSUPPORTED) and msg in ebag.last_error(), ebag.last_error()
+    assert not h.value
+
+
+def test_gemv_null_plan_rejected(lib):
+    import paper_2305_06942_amd as ebag
+    assert lib.gemv_ar_forward(None, None, None, None, None, None) == ebag.abi.EBAG_EINVAL
+    assert lib.gemv_ar_unfused_forward(None, None, None, None, None, None) == ebag.abi.EBAG_EINVAL
+    assert lib.gemv_ar_reset(None) == ebag.abi.EBAG_EINVAL
+    o = ebag.gemv_default_opts()
+    assert (o.tile_rows, o.waves_per_wg, o.comm_aware, o.debug_suppress_flag) == (64, 4, 1, -1)
+    lib.gemv_ar_destroy(None)
