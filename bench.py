@@ -441,6 +441,75 @@ def run_timeline(name, warmup):
     return out
 
 
+GEMV_SHAPES = [(16384, 8192), (32768, 8192), (65536, 8192)]  # (M outputs, K total), R = 4 ranks, fp16
+
+
+def gemv_ar_bytes(R, M, K, elt):
+    """Bytes the fused GEMV + AllReduce must move: every matrix element and
+    vector element once, each rank's partial vector written and read once
+    (the reduce-scatter) and the reduced vector written to every rank (the
+    all-gather)."""
+    return M * K * elt + K * elt + 2 * R * M * 4 + R * M * 4
+
+
+def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
+    """GEMV + AllReduce (Sec. III-B) on R logical ranks: fused (one
+    cooperative launch) against bulk-synchronous (GEMV kernel, then AllReduce
+    kernel, then flags), one JSON line per shape."""
+    import numpy as np
+    import torch
+    import paper_2305_06942_amd as ebag
+    s = torch.cuda.current_stream()
+    elt = 4 if dtype == 0 else 2
+    tdt = {0: torch.float32, 1: torch.float16, 2: torch.bfloat16}[dtype]
+    out = []
+    for M, K in shapes:
+        Ks = [K // R] * R
+        g = torch.Generator(device="cuda").manual_seed(2305 + M)
+        A = [torch.randn((M, k), generator=g, device="cuda").to(tdt) for k in Ks]
+        x = [torch.randn((k,), generator=g, device="cuda").to(tdt) for k in Ks]
+        y = [torch.empty((M,), device="cuda") for _ in range(R)]
+        plan = ebag.GemvAR(R, M, Ks, dtype)
+        P, block, n_tiles, resident = plan.launch_info()
+        flags = torch.zeros(R * P, dtype=torch.int32, device="cuda")
+        fused = lambda: plan.forward(A, x, y, flags)
+        unfused = lambda: plan.unfused_forward(A, x, y, flags)
+        for _ in range(warmup):
+            fused()
+            unfused()
+        f_ms = time_launches(fused, steps, s)
+        u_ms = time_launches(unfused, steps, s)
+        assert plan.status() == (0, -1)
+        nbytes = gemv_ar_bytes(R, M, K, elt)
+        row = {"operator": "gemv_allreduce", "ranks": R, "M": M, "K": K, "dtype": {0: "f32", 1: "f16", 2: "bf16"}[dtype],
+               "tile_rows": plan.opts.tile_rows, "wgs_per_rank": P, "threads_per_wg": block,
+               "fused_us": round(f_ms * 1e3, 2), "unfused_us": round(u_ms * 1e3, 2),
+               "fused_speedup_vs_unfused": round(u_ms / f_ms, 4), "algorithmic_bytes": nbytes,
+               "roofline": {"bound": "hbm", "achieved": round(nbytes / (f_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                            "unit": "GB/s", "frac": round(nbytes / (f_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+               "data": "synthetic: torch.randn on the device, seeded"}
+        if with_cpu and M == shapes[0][0]:
+            import oracle
+            hA = [a.cpu().numpy() if dtype != 2 else a.view(torch.int16).cpu().numpy().view(np.uint16) for a in A]
+            hx = [v.cpu().numpy() if dtype != 2 else v.view(torch.int16).cpu().numpy().view(np.uint16) for v in x]
+            times = []
+            while len(times) < 3 or sum(times) < 10.0:
+                t0 = time.time()
+                oracle.gemv_ar(hA, hx, dtype)
+                times.append(time.time() - t0)
+            med = sorted(times)[len(times) // 2]
+            row["cpu_baseline"] = {"value": round(nbytes / med / 1e9, 3), "unit": "GB/s",
+                                   "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
+                                   "sample": f"C oracle (fp64) over the whole {M} x {K} problem, median of "
+                                             f"{len(times)} passes, {med:.3f} s per pass"}
+        out.append(row)
+        print(json.dumps(row), flush=True)
+        plan.close()
+        del A, x, y, flags
+        torch.cuda.empty_cache()
+    return out
+
+
 def summarize(d):
     """Summarise rocprofv3 csv output under d: per-kernel dispatch count and
     mean / median duration, and per-kernel mean counter values."""
@@ -520,6 +589,8 @@ def main():
     ap.add_argument("--mean", action="store_true", help="mean pooling (the same bags without weights)")
     ap.add_argument("--row-probe", action="store_true", help="random-row read rate by row width")
     ap.add_argument("--per-table-slices", action="store_true", help="a ready flag per (slice, table)")
+    ap.add_argument("--gemv-ar", action="store_true", help="fused GEMV + AllReduce (Sec. III-B), several shapes")
+    ap.add_argument("--gemv-m", type=int, default=0, help="with --gemv-ar: only the shape with this M")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -544,6 +615,13 @@ def main():
         return 0
     if a.row_probe:
         run_row_probe()
+        return 0
+    if a.gemv_ar:
+        shapes = [sh for sh in GEMV_SHAPES if a.gemv_m in (0, sh[0])]
+        if not shapes:
+            print(f"bench.py: no GEMV shape with M={a.gemv_m}", file=sys.stderr)
+            return 2
+        run_gemv_ar(a.steps, a.warmup, shapes=shapes, with_cpu=not (a.no_cpu_baseline or a.profile))
         return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:

@@ -20,11 +20,14 @@
  *  - the owner's workgroup p then waits for the flags of workgroup p of every
  *    other rank, sums the R partials of its tiles in rank order and stores the
  *    result into every rank's output vector (all-gather), then adds 1 to its
- *    output flag.
+ *    output flag (reduce_mode 1).
  *
- * On one GPU the R ranks are logical: all of them run in one cooperative
- * launch (every workgroup resident at once, so the owners' waits always end),
- * and "peer memory" is a slot of a plan-owned buffer.
+ * On one GPU the R ranks are logical and "peer memory" is a slot of a
+ * plan-owned buffer.  reduce_mode 1 runs all ranks in one cooperative launch
+ * (every workgroup resident at once, so the owners' waits always end).  The
+ * default reduce_mode 0 replaces the waiting owner by an arrival counter per
+ * (owner, workgroup): whichever rank's workgroup delivers last reduces and
+ * broadcasts, so nothing waits and the kernel launches normally.
  *
  * Conventions: A[r] is row-major M x K[r] in the plan's storage type, row r
  * starting at byte i * K[r] * elt, 16-byte aligned, K[r] * elt a multiple of
@@ -55,32 +58,39 @@ extern "C" {
 typedef struct gemv_ar_plan* gemv_ar_t;
 
 typedef struct gemv_ar_opts {
-  int32_t tile_rows;           /* rows per output tile, 1..4096 (default 64) */
-  int32_t wgs_per_rank;        /* physical workgroups per rank P; 0 (default): as many as can be resident
-                                  at once for the whole grid, at most the number of tiles */
+  int32_t tile_rows;           /* rows per output tile, 1..4096 (default 128) */
+  int32_t wgs_per_rank;        /* physical workgroups per rank P, at most the number of tiles; 0 (default):
+                                  one per tile (reduce_mode 0) or as many as can be resident at once for
+                                  the whole grid (reduce_mode 1) */
   int32_t waves_per_wg;        /* wavefronts per workgroup, 1..16 (default 4) */
   int32_t comm_aware;          /* 1 (default): tiles owned by other ranks first; 0: tile order */
   int32_t debug_suppress_flag; /* >= 0: never set this peer flag ((owner * R + rank) * P + p), for
                                   failure-path tests; -1 (default) off */
-  int32_t reserved;            /* must be 0 */
-  int64_t timeout_us;          /* an owner gives up waiting after this long (default 5,000,000 us) */
+  int32_t reduce_mode;         /* 0 (default): the last of the R ranks' workgroups p to store its partials
+                                  for an owner reduces that owner's tiles (arrival counter, no waiting,
+                                  normal launch, P defaults to one tile per workgroup); 1: the owner's
+                                  workgroup waits for the peer flags and reduces (the paper's scheme;
+                                  cooperative launch, every workgroup resident) */
+  int64_t timeout_us;          /* reduce_mode 1: an owner gives up waiting after this long (default 5 s) */
 } gemv_ar_opts_t;
 
 /* Fill *opts with the defaults listed above. */
 int gemv_ar_default_opts(gemv_ar_opts_t* opts);
 
 /*
- * Create a plan on the current HIP device for R ranks (1..64), M outputs and
+ * Create a plan on the current HIP device for R ranks (1..16), M outputs and
  * K[r] columns per rank (host array of R values, each > 0 with K[r] * elt a
- * multiple of 16), storage type dtype.  The plan owns the reduction slots
- * (R * M floats), the peer flags and a status word.
+ * multiple of 16, K[r] * elt at most 64 KiB), storage type dtype.  The plan
+ * owns the reduction slots (R * M floats), the peer flags, the arrival
+ * counters and a status word.  One forward may be in flight per plan.
  */
 int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_dtype_t dtype,
                    const gemv_ar_opts_t* opts);
 
-/* Fused forward: one cooperative launch computing y[r] = sum_s A_s x_s for
- * every rank r.  A, x, y: host arrays of R device pointers.  out_flags: NULL
- * or device uint32 [R * P] (P from gemv_ar_launch_info). */
+/* Fused forward: one launch (cooperative with reduce_mode 1) computing
+ * y[r] = sum_s A_s x_s for every rank r.  A, x, y: host arrays of R device
+ * pointers.  out_flags: NULL or device uint32 [R * P] (P from
+ * gemv_ar_launch_info). */
 int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, float* const* y,
                     uint32_t* out_flags, hipStream_t stream);
 

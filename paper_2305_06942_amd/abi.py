@@ -45,7 +45,7 @@ class GemvOpts(ctypes.Structure):
         ("waves_per_wg", ctypes.c_int32),
         ("comm_aware", ctypes.c_int32),
         ("debug_suppress_flag", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("reduce_mode", ctypes.c_int32),
         ("timeout_us", ctypes.c_int64),
     ]
 

@@ -2,17 +2,22 @@
 // baseline; the C ABI is declared in include/gemv_ar.h.
 //
 // GEMV: a wave computes rows of its tile; for a row, lane l takes the 16-byte
-// vectors l, l + 64, ... of the row (coalesced loads, UJ per lane in flight,
-// two rows at a time) and the matching vectors of x from LDS, where the
+// vectors l, l + 64, ... of the row (coalesced non-temporal loads -- the
+// matrix is read once --, UJ per lane and row in flight, RPI rows at a time)
+// and the matching vectors of x from LDS, where the
 // workgroup staged its rank's x once.  Products are accumulated in fp32 per
 // lane and combined with xor shuffles.
 //
-// AllReduce (fused): two-phase direct algorithm.  Workgroup (r, p) stores its
-// partial tiles for owner q into the reduction slots part[r][rows] with
-// device-scope stores, waits for them to complete and sets peer flag
-// (q, r, p) to the forward's epoch.  Owner workgroup (q, p) polls the flags
-// of (s, p) for every s != q, sums part[0..R-1][rows] in rank order with
-// device-scope loads and stores the result into every rank's output.
+// AllReduce (fused), two-phase direct: workgroup (r, p) stores its partial
+// tiles for owner q into the reduction slots part[r][rows] with device-scope
+// stores and waits for them to complete.  Then either
+//  - owner-waits mode (the paper's scheme, cooperative launch): it sets peer
+//    flag (q, r, p) to the forward's epoch, and owner workgroup (q, p) polls
+//    the flags of (s, p) for every s != q before reducing; or
+//  - last-arriver mode (default): it counts itself in on counter (q, p), and
+//    the workgroup completing the count reduces.
+// The reduction sums part[0..R-1][rows] in rank order with device-scope loads
+// and stores the result into every rank's output.
 #include <climits>
 #include <cstring>
 #include <new>
@@ -26,6 +31,7 @@ namespace {
 
 constexpr int kMaxRanks = 16;
 constexpr int UJ = 4;             // 16-byte loads in flight per lane per row
+constexpr int RPI = 4;            // rows a wave works on at once (RPI * UJ loads in flight per lane)
 constexpr int kMaxXBytes = 64 * 1024;
 
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
@@ -37,7 +43,8 @@ struct GemvArgs {
   float* y[kMaxRanks];
   int64_t K[kMaxRanks];
   float* part;           // [R][M] partial vectors (the owners' reduction slots)
-  uint32_t* peer;        // [R owner][R source][P] epoch flags
+  uint32_t* peer;        // [R owner][R source][P] epoch flags (owner-waits mode)
+  uint32_t* cnt;         // [R owner][P] arrival counters (last-arriver mode, self-resetting)
   uint32_t* out_flags;   // [R][P] or nullptr
   int32_t* status;       // [2]: timed out, first missing peer flag
   int64_t M;
@@ -133,21 +140,26 @@ __device__ void partial_tile(const GemvArgs& a, int r, int64_t tile, const u4v* 
   for (int base = r0; base < r1; base += 64) {  // results of up to 64 rows per store
     float res = 0.f;
     const int nb = min(64, r1 - base);
-    for (int k = 0; k < nb; k += 2) {
-      const bool two = k + 1 < nb;
-      const char* pa = Ar + (row0 + base + k) * row_bytes;
-      const char* pb = two ? pa + row_bytes : pa;
-      float acc0 = 0.f, acc1 = 0.f;
+    for (int k = 0; k < nb; k += RPI) {
+      const char* pr[RPI];
+      bool has[RPI];
+#pragma unroll
+      for (int j = 0; j < RPI; ++j) {
+        has[j] = k + j < nb;
+        pr[j] = Ar + (row0 + base + k + (has[j] ? j : 0)) * row_bytes;
+      }
+      float acc[RPI];
+#pragma unroll
+      for (int j = 0; j < RPI; ++j) acc[j] = 0.f;
       for (int v0 = 0; v0 < V; v0 += 64 * UJ) {
-        u4v ra[UJ], rb[UJ];
+        u4v ra[RPI][UJ];
 #pragma unroll
         for (int u = 0; u < UJ; ++u) {
           const int v = v0 + u * 64 + lane;
-          ra[u] = u4v{0u, 0u, 0u, 0u};
-          rb[u] = u4v{0u, 0u, 0u, 0u};
-          if (v < V) {
-            ra[u] = *(gu4v*)(pa + (int64_t)v * 16);
-            if (two) rb[u] = *(gu4v*)(pb + (int64_t)v * 16);
+#pragma unroll
+          for (int j = 0; j < RPI; ++j) {
+            ra[j][u] = u4v{0u, 0u, 0u, 0u};
+            if (v < V && has[j]) ra[j][u] = __builtin_nontemporal_load((gu4v*)(pr[j] + (int64_t)v * 16));
           }
         }
 #pragma unroll
@@ -155,18 +167,19 @@ __device__ void partial_tile(const GemvArgs& a, int r, int64_t tile, const u4v* 
           const int v = v0 + u * 64 + lane;
           if (v < V) {
             const u4v xv = lds_x[v];
-            acc0 += dot16<DT>(ra[u], xv);
-            acc1 += dot16<DT>(rb[u], xv);
+#pragma unroll
+            for (int j = 0; j < RPI; ++j) acc[j] += dot16<DT>(ra[j][u], xv);
           }
         }
       }
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) {
-        acc0 += __shfl_xor(acc0, m);
-        acc1 += __shfl_xor(acc1, m);
+#pragma unroll
+        for (int j = 0; j < RPI; ++j) acc[j] += __shfl_xor(acc[j], m);
       }
-      if (lane == k) res = acc0;
-      if (two && lane == k + 1) res = acc1;
+#pragma unroll
+      for (int j = 0; j < RPI; ++j)
+        if (has[j] && lane == k + j) res = acc[j];
     }
     if (lane < nb) store_f32(out + base + lane, res, device_scope);
   }
@@ -180,6 +193,68 @@ __device__ __forceinline__ int64_t first_tile(int64_t t0, int p, int P) {
 
 // Tiles owned by rank q: [ceil(q * n / R), ceil((q + 1) * n / R)).
 __device__ __forceinline__ int64_t owner_begin(int64_t n, int q, int R) { return (q * n + R - 1) / R; }
+
+// Sum the R partials of owner q's tiles handled by workgroup p (rank order,
+// device-scope loads) and store the result into every rank's output.
+__device__ void reduce_owned(const GemvArgs& a, int q, int p) {
+  const int64_t t0 = owner_begin(a.n_tiles, q, a.R), t1 = owner_begin(a.n_tiles, q + 1, a.R);
+  for (int64_t i = first_tile(t0, p, a.P); i < t1; i += a.P) {
+    const int64_t row0 = i * a.TM;
+    const int nrows = (int)min((int64_t)a.TM, a.M - row0);
+    for (int k = threadIdx.x; k < nrows; k += blockDim.x) {
+      float sum = 0.f;
+      for (int s = 0; s < a.R; ++s) sum += load_f32_device(a.part + (int64_t)s * a.M + row0 + k);
+      for (int r = 0; r < a.R; ++r) store_f32(a.y[r] + row0 + k, sum, true);
+    }
+  }
+}
+
+// Fused kernel, last-arriver reduction (default): workgroup (r, p) computes
+// its partial tiles owner by owner; after each owner's tiles are stored it
+// counts itself in on that owner's counter (q, p), and the workgroup that
+// completes the count -- the last of the R ranks to deliver -- reduces and
+// broadcasts the owner's tiles, then re-arms the counter.  Nobody waits, so
+// the grid needs no co-residency and launches normally.
+template <int DT>
+__global__ __launch_bounds__(1024) void gemv_ar_last_arriver_kernel(const GemvArgs a) {
+  extern __shared__ u4v lds_x[];
+  __shared__ uint32_t s_old;
+  const int r = blockIdx.x / a.P;
+  const int p = blockIdx.x - r * a.P;
+  stage_x(a.x[r], a.K[r] * (DT == 0 ? 4 : 2), lds_x);
+  __syncthreads();
+  for (int qi = 0; qi < a.R; ++qi) {
+    const int q = a.comm_aware ? (r + 1 + qi) % a.R : qi;
+    const int64_t t0 = owner_begin(a.n_tiles, q, a.R), t1 = owner_begin(a.n_tiles, q + 1, a.R);
+    const int64_t i0 = first_tile(t0, p, a.P);
+    if (i0 >= t1) {
+      // No tile of owner q for workgroup p (on every rank alike): the owner's
+      // own workgroup advances the output flag, which has nothing to cover.
+      if (q == r && a.out_flags && threadIdx.x == 0)
+        __hip_atomic_fetch_add(&a.out_flags[(int64_t)q * a.P + p], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      continue;
+    }
+    for (int64_t i = i0; i < t1; i += a.P) partial_tile<DT>(a, r, i, lds_x, true);
+    // every wave's partial stores complete (device scope) before counting in
+    wait_all_memory();
+    __syncthreads();
+    uint32_t* c = &a.cnt[(int64_t)q * a.P + p];
+    if (threadIdx.x == 0) s_old = __hip_atomic_fetch_add(c, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (s_old == (uint32_t)a.R - 1) {
+      reduce_owned(a, q, p);
+      wait_all_memory();
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        __hip_atomic_store(c, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.out_flags)
+          __hip_atomic_fetch_add(&a.out_flags[(int64_t)q * a.P + p], 1u, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    __syncthreads();  // s_old is rewritten for the next owner
+  }
+}
 
 template <int DT>
 __global__ __launch_bounds__(1024) void gemv_ar_fused_kernel(const GemvArgs a) {
@@ -226,16 +301,7 @@ __global__ __launch_bounds__(1024) void gemv_ar_fused_kernel(const GemvArgs a) {
   __syncthreads();
   if (s_bad) return;
   // Reduce the owned tiles in rank order and store them to every rank.
-  const int64_t t0 = owner_begin(a.n_tiles, r, a.R), t1 = owner_begin(a.n_tiles, r + 1, a.R);
-  for (int64_t i = first_tile(t0, p, a.P); i < t1; i += a.P) {
-    const int64_t row0 = i * a.TM;
-    const int nrows = (int)min((int64_t)a.TM, a.M - row0);
-    for (int k = threadIdx.x; k < nrows; k += blockDim.x) {
-      float sum = 0.f;
-      for (int s = 0; s < a.R; ++s) sum += load_f32_device(a.part + (int64_t)s * a.M + row0 + k);
-      for (int q = 0; q < a.R; ++q) store_f32(a.y[q] + row0 + k, sum, true);
-    }
-  }
+  reduce_owned(a, r, p);
   if (a.out_flags) {
     wait_all_memory();
     __syncthreads();
@@ -275,6 +341,10 @@ typedef void (*gemv_fn)(const GemvArgs);
 gemv_fn fused_fn(int dt) {
   return dt == 0 ? gemv_ar_fused_kernel<0> : dt == 1 ? gemv_ar_fused_kernel<1> : gemv_ar_fused_kernel<2>;
 }
+gemv_fn last_arriver_fn(int dt) {
+  return dt == 0 ? gemv_ar_last_arriver_kernel<0>
+                 : dt == 1 ? gemv_ar_last_arriver_kernel<1> : gemv_ar_last_arriver_kernel<2>;
+}
 gemv_fn partial_fn(int dt) {
   return dt == 0 ? gemv_partial_kernel<0> : dt == 1 ? gemv_partial_kernel<1> : gemv_partial_kernel<2>;
 }
@@ -302,6 +372,7 @@ struct gemv_ar_plan {
   uint32_t epoch = 0;
   float* d_part = nullptr;
   uint32_t* d_peer = nullptr;
+  uint32_t* d_cnt = nullptr;
   int32_t* d_status = nullptr;
 };
 
@@ -313,6 +384,7 @@ void free_gemv(gemv_ar_plan* h) {
   if (!h) return;
   (void)hipFree(h->d_part);
   (void)hipFree(h->d_peer);
+  (void)hipFree(h->d_cnt);
   (void)hipFree(h->d_status);
   delete h;
 }
@@ -336,6 +408,7 @@ int fill_args(gemv_ar_plan* h, const void* const* A, const void* const* x, float
   }
   a->part = h->d_part;
   a->peer = h->d_peer;
+  a->cnt = h->d_cnt;
   a->out_flags = out_flags;
   a->status = h->d_status;
   a->M = h->M;
@@ -356,11 +429,12 @@ extern "C" {
 int gemv_ar_default_opts(gemv_ar_opts_t* o) {
   if (!o) return fail(EBAG_EINVAL, "null opts");
   std::memset(o, 0, sizeof *o);
-  o->tile_rows = 64;
+  o->tile_rows = 128;
   o->wgs_per_rank = 0;
   o->waves_per_wg = 4;
   o->comm_aware = 1;
   o->debug_suppress_flag = -1;
+  o->reduce_mode = 0;
   o->timeout_us = 5000000;
   return EBAG_OK;
 }
@@ -379,7 +453,7 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   if (o.waves_per_wg < 1 || o.waves_per_wg > 16) return fail(EBAG_EINVAL, "waves_per_wg must be in [1, 16]");
   if (o.wgs_per_rank < 0) return fail(EBAG_EINVAL, "wgs_per_rank must be >= 0");
   if (o.comm_aware != 0 && o.comm_aware != 1) return fail(EBAG_EINVAL, "comm_aware must be 0 or 1");
-  if (o.reserved != 0) return fail(EBAG_EINVAL, "reserved option field must be 0");
+  if (o.reduce_mode != 0 && o.reduce_mode != 1) return fail(EBAG_EINVAL, "reduce_mode must be 0 or 1");
   if (o.timeout_us < 1) return fail(EBAG_EINVAL, "timeout_us must be >= 1");
   const int elt = dtype == EBAG_F32 ? 4 : 2;
   int64_t max_x = 0;
@@ -407,17 +481,22 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   if (e == hipSuccess && hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, h->device) == hipSuccess &&
       khz > 0)
     h->ticks_per_us = khz / 1000.0;
+  const bool owner_mode = o.reduce_mode == 1;
   int per_cu = 0;
   if (e == hipSuccess)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fused_fn(h->dtype), h->block, (size_t)max_x);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, owner_mode ? fused_fn(h->dtype) : last_arriver_fn(h->dtype), h->block, (size_t)max_x);
   if (e != hipSuccess) {
     free_gemv(h);
     return hipf(e, "query device");
   }
   h->resident = per_cu * h->num_cus;
-  int64_t P = o.wgs_per_rank > 0 ? o.wgs_per_rank : h->resident / R;
+  // Owner-waits mode needs every workgroup resident (cooperative launch);
+  // the last-arriver mode does not and defaults to one tile per workgroup.
+  int64_t P = o.wgs_per_rank > 0 ? o.wgs_per_rank : owner_mode ? h->resident / R : h->n_tiles;
   if (P > h->n_tiles) P = h->n_tiles;
-  if (P < 1 || P * R > h->resident) {
+  if (P * R > INT_MAX) P = INT_MAX / R;
+  if (P < 1 || (owner_mode && P * R > h->resident)) {
     const int rc = fail(EBAG_EUNSUPPORTED, "%lld workgroups per rank x %d ranks cannot all be resident (%d fit)",
                         (long long)P, R, h->resident);
     free_gemv(h);
@@ -436,6 +515,8 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   GEMV_TRY(hipMalloc((void**)&h->d_part, sizeof(float) * (size_t)R * (size_t)M), "alloc reduction slots");
   GEMV_TRY(hipMalloc((void**)&h->d_peer, sizeof(uint32_t) * (size_t)R * R * P), "alloc peer flags");
   GEMV_TRY(hipMemset(h->d_peer, 0, sizeof(uint32_t) * (size_t)R * R * P), "zero peer flags");
+  GEMV_TRY(hipMalloc((void**)&h->d_cnt, sizeof(uint32_t) * (size_t)R * P), "alloc arrival counters");
+  GEMV_TRY(hipMemset(h->d_cnt, 0, sizeof(uint32_t) * (size_t)R * P), "zero arrival counters");
   GEMV_TRY(hipMalloc((void**)&h->d_status, sizeof(kGemvStatusInit)), "alloc status");
   GEMV_TRY(hipMemcpy(h->d_status, kGemvStatusInit, sizeof(kGemvStatusInit), hipMemcpyHostToDevice), "init status");
 #undef GEMV_TRY
@@ -453,6 +534,13 @@ int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, flo
   // Epoch 0 is the value the flags start from, so it is skipped.
   if (++h->epoch == 0) ++h->epoch;
   a.epoch = h->epoch;
+  if (h->opts.reduce_mode == 0) {
+    hipLaunchKernelGGL(last_arriver_fn(h->dtype), dim3((unsigned)(h->R * h->P)), dim3(h->block),
+                       (size_t)h->max_x_bytes, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hipf(e, "launch the fused GEMV + AllReduce kernel");
+    return EBAG_OK;
+  }
   void* args[] = {&a};
   const hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fused_fn(h->dtype)),
                                                   dim3((unsigned)(h->R * h->P)), dim3(h->block), args,

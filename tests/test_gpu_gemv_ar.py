@@ -66,7 +66,7 @@ def _run(R, M, Ks, dtype, seed, integer=False, epochs=2, **opts):
     dx = [_to_dev(v, dtype) for v in x]
     plan = ebag.GemvAR(R, M, Ks, dtype, **opts)
     P, block, n_tiles, resident = plan.launch_info()
-    assert 1 <= P <= n_tiles and R * P <= resident
+    assert 1 <= P <= n_tiles and (opts.get("reduce_mode", 0) == 0 or R * P <= resident)
     rel = _depth(R, Ks, dtype) * 2.0 ** -24
     outs = []
     for fused in (True, False):
@@ -91,31 +91,36 @@ def _run(R, M, Ks, dtype, seed, integer=False, epochs=2, **opts):
     plan.close()
 
 
+@pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("dtype", [synth.F32, synth.F16, synth.BF16])
 @pytest.mark.parametrize("R", [1, 2, 4, 8])
-def test_gemv_ar_parity(dtype, R):
+def test_gemv_ar_parity(dtype, R, mode):
     elt = 4 if dtype == synth.F32 else 2
     Ks = [(16 // elt) * k for k in ([37, 64, 5, 129, 256, 16, 3, 200][:R])]
-    _run(R, 3000 + 37, Ks, dtype, seed=R * 3 + dtype)
+    _run(R, 3000 + 37, Ks, dtype, seed=R * 3 + dtype, reduce_mode=mode)
 
 
+@pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("dtype", [synth.F32, synth.F16, synth.BF16])
-def test_gemv_ar_integer_exact(dtype):
+def test_gemv_ar_integer_exact(dtype, mode):
     elt = 4 if dtype == synth.F32 else 2
-    _run(4, 2048 + 5, [(16 // elt) * k for k in (64, 32, 100, 8)], dtype, seed=7, integer=True)
+    _run(4, 2048 + 5, [(16 // elt) * k for k in (64, 32, 100, 8)], dtype, seed=7, integer=True, reduce_mode=mode)
 
 
+@pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("opts", [dict(tile_rows=1), dict(tile_rows=16), dict(tile_rows=1000),
                                   dict(wgs_per_rank=1), dict(wgs_per_rank=3), dict(comm_aware=0),
                                   dict(waves_per_wg=1), dict(waves_per_wg=16)],
                          ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()))
-def test_gemv_ar_launch_options(opts):
-    _run(4, 1500, [512, 256, 1024, 128], synth.F16, seed=11, **opts)
+def test_gemv_ar_launch_options(opts, mode):
+    _run(4, 1500, [512, 256, 1024, 128], synth.F16, seed=11, reduce_mode=mode, **opts)
 
 
-def test_gemv_ar_benchmark_shape():
-    """The benchmarked shape: M = 32768 outputs, K = 8192 over 4 ranks, fp16."""
-    _run(4, 32768, [2048] * 4, synth.F16, seed=13, epochs=1)
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("M", [16384, 32768, 65536])
+def test_gemv_ar_benchmark_shapes(M, mode):
+    """The benchmarked shapes: M outputs, K = 8192 over 4 ranks, fp16."""
+    _run(4, M, [2048] * 4, synth.F16, seed=13, epochs=2, reduce_mode=mode)
 
 
 def test_gemv_ar_suppressed_peer_flag_times_out():
@@ -130,7 +135,8 @@ def test_gemv_ar_suppressed_peer_flag_times_out():
     dA = [_to_dev(a, dtype) for a in A]
     dx = [_to_dev(v, dtype) for v in x]
     f = (1 * R + 0) * P + 0  # owner 1, source rank 0, workgroup 0
-    plan = ebag.GemvAR(R, M, Ks, dtype, wgs_per_rank=P, debug_suppress_flag=f, timeout_us=20000)
+    plan = ebag.GemvAR(R, M, Ks, dtype, tile_rows=64, wgs_per_rank=P, debug_suppress_flag=f, timeout_us=20000,
+                       reduce_mode=1)
     assert plan.launch_info()[0] == P and plan.launch_info()[2] == 16
     y = [torch.full((M,), float("nan"), device="cuda") for _ in range(R)]
     plan.forward(dA, dx, y)
