@@ -58,6 +58,8 @@ def load(path: str = LIB):
     lib.oracle_validate.restype = ctypes.c_int
     lib.oracle_flags.argtypes = [i64, i32, i32, i32, ctypes.c_uint32, P, i64]
     lib.oracle_flags.restype = ctypes.c_int
+    lib.oracle_backward.argtypes = [i32, P, P, P, i32, i64, i32, P, P]
+    lib.oracle_backward.restype = ctypes.c_int
     lib.oracle_gemv_ar.argtypes = [i32, i64, P, i32, P, P, P, P, P, i32]
     lib.oracle_gemv_ar.restype = ctypes.c_int
     lib.oracle_half_to_double.argtypes = [ctypes.c_uint16]
@@ -129,6 +131,26 @@ def flags(B, R, C, epoch, lib=None, per_slice=1):
     if rc != 0:
         raise OracleError(f"oracle_flags: {ERRORS.get(rc, rc)}")
     return out
+
+
+def backward(dims, offsets, weights, grad, B, R, mean=False, lib=None):
+    """Embedding backward: per-lookup gradient rows (lookup order, table
+    blocks one after the other) from the pooled-output gradient ``grad``
+    ([B][sum D] fp32, the destination-partitioned layout).  Returns a flat
+    fp32 array of sum over t of nnz_t * D_t values."""
+    lib = lib or load()
+    dims = np.ascontiguousarray(dims, dtype=np.int32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int64)
+    grad = np.ascontiguousarray(grad, dtype=np.float32)
+    weights = None if weights is None else np.ascontiguousarray(weights, dtype=np.float32)
+    T = dims.size
+    n = int(sum((offsets[(t + 1) * B] - offsets[t * B]) * dims[t] for t in range(T)))
+    values = np.empty(max(n, 1), dtype=np.float32)
+    rc = lib.oracle_backward(T, dims.ctypes.data, offsets.ctypes.data, _ptr(weights), int(bool(mean)), B, R,
+                             grad.ctypes.data, values.ctypes.data)
+    if rc != 0:
+        raise OracleError(f"oracle_backward: {ERRORS.get(rc, rc)}")
+    return values[:n]
 
 
 def gemv_ar(A, x, dtype, nthreads=None, lib=None):

@@ -279,3 +279,57 @@ int oracle_gemv_ar(int32_t R, int64_t M, const int64_t* Ks, int32_t dtype, const
   free(jobs);
   return OR_OK;
 }
+
+/*
+ * Embedding backward (the backward counterpart of the pooling above, which
+ * the paper overlaps with its All-to-All as well, Sec. IV-D): the owner of
+ * the tables receives the gradient of every pooled vector in the same
+ * destination-partitioned layout, grad[R][S][sum D] (= [B][sum D]).  The
+ * gradient of lookup k of bag (t, b) -- the row indices[k] contributed once
+ * to that bag -- is
+ *   sum mode:   w_k * grad[b][off_t .. off_t + D_t)   (w_k = 1 without weights)
+ *   mean mode:  grad[b][off_t .. off_t + D_t) / L      (L = the bag's length)
+ * Output: for each table, in lookup order, a block of nnz_t rows of D_t
+ * fp32 values; the blocks follow each other in table order (table t starts
+ * at sum over t' < t of nnz_t' * D_t' floats).  Each value is the exact
+ * result rounded to fp32 once (fp32 x fp32 products and quotients by L are
+ * computed exactly enough in fp64 for that rounding to be the correct one).
+ */
+int oracle_backward(int32_t T, const int32_t* dims, const int64_t* offsets, const float* weights, int32_t mode,
+                    int64_t B, int32_t R, const float* grad, float* values) {
+  if (T <= 0 || B <= 0 || R <= 0 || !dims || !offsets || !grad || !values) return OR_BAD_ARGS;
+  if (mode < 0 || mode > 1 || (mode == 1 && weights)) return OR_BAD_ARGS;
+  if (B % R != 0) return OR_BAD_SPLIT;
+  if (offsets[0] != 0) return OR_BAD_OFFSETS;
+  for (int64_t q = 0; q < (int64_t)T * B; ++q)
+    if (offsets[q + 1] < offsets[q]) return OR_BAD_OFFSETS;
+  int64_t sum_dim = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    if (dims[t] <= 0) return OR_BAD_ARGS;
+    sum_dim += dims[t];
+  }
+  int64_t block = 0;  /* first float of table t's block */
+  int64_t col = 0;    /* off_t */
+  for (int32_t t = 0; t < T; ++t) {
+    const int64_t D = dims[t];
+    const int64_t first = offsets[(int64_t)t * B];
+    for (int64_t b = 0; b < B; ++b) {
+      const int64_t lo = offsets[(int64_t)t * B + b], hi = offsets[(int64_t)t * B + b + 1];
+      const float* g = grad + b * sum_dim + col; /* [B][sum D] row b = send[r][s] with b = r * S + s */
+      for (int64_t k = lo; k < hi; k++) {
+        float* out = values + block + (k - first) * D;
+        for (int64_t j = 0; j < D; ++j) {
+          double v = (double)g[j];
+          if (mode == 1)
+            v = v / (double)(hi - lo);
+          else if (weights)
+            v = (double)weights[k] * v;
+          out[j] = (float)v;
+        }
+      }
+    }
+    block += (offsets[(int64_t)(t + 1) * B] - first) * D;
+    col += D;
+  }
+  return OR_OK;
+}

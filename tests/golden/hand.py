@@ -70,3 +70,24 @@ def load_gemv(path=GEMV_PATH):
     d["A"] = [np.array(A[r]) for r in range(R)]
     d["x"] = [np.array(x[r]) for r in range(R)]
     return d
+
+
+BACKWARD_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "backward_hand.txt")
+
+
+def load_backward(path=BACKWARD_PATH):
+    """Parse the hand-worked backward fixture: the pooled gradient rows and
+    the expected per-lookup rows (exact rationals rounded once to fp32) for
+    the sum, weighted-sum and mean modes."""
+    d = {"grad": [], "sum": [], "wsum": [], "mean": []}
+    with open(path) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            key, *rest = line.split()
+            d[key].append([float(fractions.Fraction(v)) for v in rest])
+    out = {"grad": np.array(d["grad"], dtype=np.float32)}
+    for k in ("sum", "wsum", "mean"):
+        out[k] = np.array(d[k], dtype=np.float64).astype(np.float32)
+    return out

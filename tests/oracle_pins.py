@@ -414,7 +414,77 @@ def pin_gemv_validation(lib):
             raise AssertionError("shape mismatch accepted")
 
 
+# ---- Embedding backward -----------------------------------------------------
+
+
+def pin_backward_hand(lib):
+    d = hand.load()
+    bw = hand.load_backward()
+    off = np.array(d["offsets"], dtype=np.int64)
+    w = np.array(d["weights"], dtype=np.float32)
+    dims = [4, 4]
+    for key, weights, mean in (("sum", None, False), ("wsum", w, False), ("mean", None, True)):
+        got = oracle.backward(dims, off, weights, bw["grad"], d["B"], d["R"], mean=mean, lib=lib)
+        assert np.array_equal(got.reshape(-1, 4), bw[key]), key
+
+
+def pin_backward_torch(lib):
+    """Special case that reduces to a library routine: scattering the
+    per-lookup rows onto their table rows gives the dense gradient that
+    torch's autograd computes for F.embedding_bag (sum, weighted sum, mean)."""
+    import torch
+    import torch.nn.functional as F
+    rng = np.random.default_rng(43)
+    T, B, R = 3, 24, 4
+    rows, dims = [50, 9, 70], [8, 16, 4]
+    off, idx = _random_bags(rng, T, B, rows, 30, allow_empty=True)
+    grad = rng.standard_normal((B, sum(dims))).astype(np.float32)
+    w = rng.random(off[-1], dtype=np.float32)
+    for weights, mean in ((None, False), (w, False), (None, True)):
+        vals = oracle.backward(dims, off, weights, grad, B, R, mean=mean, lib=lib).astype(np.float64)
+        base, col = 0, 0
+        for t in range(T):
+            a, b = off[t * B], off[(t + 1) * B]
+            tab = torch.zeros((rows[t], dims[t]), dtype=torch.float64, requires_grad=True)
+            psw = None if weights is None else torch.from_numpy(weights[a:b].astype(np.float64))
+            out = F.embedding_bag(torch.from_numpy(idx[a:b].astype(np.int64)), tab,
+                                  torch.from_numpy((off[t * B:(t + 1) * B] - a).astype(np.int64)),
+                                  mode="mean" if mean else "sum", per_sample_weights=psw)
+            out.backward(torch.from_numpy(grad[:, col:col + dims[t]].astype(np.float64)))
+            mine = np.zeros((rows[t], dims[t]))
+            np.add.at(mine, idx[a:b], vals[base:base + (b - a) * dims[t]].reshape(b - a, dims[t]))
+            assert np.allclose(mine, tab.grad.numpy(), rtol=1e-6, atol=1e-6), (t, mean, weights is None)
+            base += (b - a) * dims[t]
+            col += dims[t]
+
+
+def pin_backward_closed_forms(lib):
+    """A constant pooled gradient c: every plain row is c, every mean row c/L,
+    every weighted row c * w_k (single fp32 rounding each)."""
+    rng = np.random.default_rng(47)
+    T, B, R = 2, 12, 3
+    rows, dims = [20, 20], [8, 4]
+    off, idx = _random_bags(rng, T, B, rows, 20, allow_empty=True)
+    c = np.float32(0.7)
+    grad = np.full((B, sum(dims)), c, dtype=np.float32)
+    w = rng.random(off[-1], dtype=np.float32)
+    plain = oracle.backward(dims, off, None, grad, B, R, lib=lib)
+    assert np.all(plain == c)
+    wv = oracle.backward(dims, off, w, grad, B, R, lib=lib)
+    mv = oracle.backward(dims, off, None, grad, B, R, mean=True, lib=lib)
+    base = 0
+    for t in range(T):
+        for b in range(B):
+            lo, hi = off[t * B + b], off[t * B + b + 1]
+            for k in range(lo, hi):
+                seg = slice(base + (k - off[t * B]) * dims[t], base + (k - off[t * B] + 1) * dims[t])
+                assert np.all(wv[seg] == np.float32(np.float64(w[k]) * np.float64(c)))
+                assert np.all(mv[seg] == np.float32(np.float64(c) / (hi - lo)))
+        base += (off[(t + 1) * B] - off[t * B]) * dims[t]
+
+
 ALL_PINS = [pin_hand, pin_integer_exact, pin_ones_and_weights, pin_row_coded, pin_placement,
             pin_fp16_decode, pin_bf16_decode, pin_fp16_pool, pin_torch_embedding_bag, pin_mean_closed_forms,
             pin_torch_embedding_bag_mean, pin_validation, pin_gemv_hand, pin_gemv_integer_exact, pin_gemv_matmul,
-            pin_gemv_closed_forms, pin_gemv_validation]
+            pin_gemv_closed_forms, pin_gemv_validation, pin_backward_hand, pin_backward_torch,
+            pin_backward_closed_forms]

@@ -37,6 +37,10 @@ MUTANTS = {
     "gemv_x_reversed": ("load_elem(J->x[r], J->dtype, k)", "load_elem(J->x[r], J->dtype, K - 1 - k)"),
     "gemv_abs_not_abs": ("mag = mag + fabs(term);", "mag = mag + term;"),
     "gemv_no_rounding_to_f32": ("if (J->y) J->y[i] = (float)sum;", "if (J->y) J->y[i] = (float)(sum + 1e-3);"),
+    "backward_no_weight": ("            v = (double)weights[k] * v;", "            v = v;"),
+    "backward_mean_off_by_one": ("            v = v / (double)(hi - lo);", "            v = v / (double)(hi - lo + 1);"),
+    "backward_block_start": ("    block += (offsets[(int64_t)(t + 1) * B] - first) * D;", "    block += (offsets[(int64_t)(t + 1) * B] - first) * D - D;"),
+    "backward_column": ("      const float* g = grad + b * sum_dim + col;", "      const float* g = grad + b * sum_dim;"),
     "round_down": ("if (J->send) J->send[out + j] = (float)sum;", "if (J->send) J->send[out + j] = (float)floor(sum);"),
 }
 
