@@ -441,6 +441,77 @@ def run_timeline(name, warmup):
     return out
 
 
+def backward_bytes(w, lengths, weighted):
+    """Bytes the embedding backward must move: every per-lookup row written,
+    the pooled gradient read once, the CSR offsets, and the weights."""
+    L = lengths.reshape(w.T, w.B).sum(axis=1)
+    rows = int(sum(int(L[t]) * w.dims[t] * 4 for t in range(w.T)))
+    nnz = int(L.sum())
+    return rows + 4 * w.B * w.sum_dim + 8 * (w.T * w.B + 1) + (4 * nnz if weighted else 0)
+
+
+def run_backward(name, steps, warmup):
+    """Embedding backward: the kernel alone (gradient complete), the
+    bulk-synchronous sequence (delivery of the gradient, then the backward)
+    and the fused one (backward expanding slices as the delivery lands)."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    w, inp, dev, _, _ = _setup(name)
+    opts = dict(PLAN_OPTS.get(name, {}))
+    opts.pop("stream_rows", None)
+    opts.pop("persistent_wgs_per_cu", None)
+    plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **opts)
+    n_vals = int(sum((inp.offsets[(t + 1) * w.B] - inp.offsets[t * w.B]) * w.dims[t] for t in range(w.T)))
+    values = torch.empty((n_vals,), device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(2305)
+    grad_dp = torch.randn((w.B, w.sum_dim), generator=g, device="cuda")
+    grad_recv = torch.empty_like(grad_dp)
+    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    s = torch.cuda.current_stream()
+    nbytes = backward_bytes(w, inp.lengths, inp.weights is not None)
+    bwd = lambda: plan.backward(grad_recv, dev.offsets, dev.weights, w.B, w.R, values)
+    for _ in range(warmup):
+        bwd()
+    k_ms = time_launches(bwd, steps, s)
+    epoch = [0]
+    send_q, bwd_q = ebag.queue_stream(), ebag.queue_stream()
+
+    def sequence(fused):
+        ev0, ev1, ev2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        times = []
+        for it in range(warmup + steps):
+            send_q.wait_stream(s)
+            ev0.record(send_q)
+            bwd_q.wait_event(ev0)
+            epoch[0] += 1
+            with torch.cuda.stream(send_q):
+                plan.deliver(grad_dp, grad_recv, flags, w.B, w.R)
+            if not fused:
+                bwd_q.wait_stream(send_q)
+            with torch.cuda.stream(bwd_q):
+                plan.backward(grad_recv, dev.offsets, dev.weights, w.B, w.R, values,
+                              grad_flags=flags if fused else None, expected_epoch=epoch[0])
+            ev1.record(send_q)
+            ev2.record(bwd_q)
+            torch.cuda.synchronize()
+            if it >= warmup:
+                times.append(max(ev0.elapsed_time(ev1), ev0.elapsed_time(ev2)))
+        assert plan.status_ex() == (0, -1, 0, -1)
+        return sorted(times)[len(times) // 2]
+    f_ms = sequence(True)
+    u_ms = sequence(False)
+    row = {"operator": "embedding_backward", "workload": name, "values_bytes": 4 * n_vals,
+           "algorithmic_bytes": nbytes, "kernel_us": round(k_ms * 1e3, 2),
+           "fused_with_delivery_us": round(f_ms * 1e3, 2), "delivery_then_backward_us": round(u_ms * 1e3, 2),
+           "fused_speedup": round(u_ms / f_ms, 4),
+           "roofline": {"bound": "hbm", "achieved": round(nbytes / (k_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(nbytes / (k_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+           "data": "synthetic: the workload's bags, a seeded torch.randn pooled gradient"}
+    print(json.dumps(row), flush=True)
+    plan.close()
+    return row
+
+
 GEMV_SHAPES = [(16384, 8192), (32768, 8192), (65536, 8192)]  # (M outputs, K total), R = 4 ranks, fp16
 
 
@@ -591,6 +662,7 @@ def main():
     ap.add_argument("--per-table-slices", action="store_true", help="a ready flag per (slice, table)")
     ap.add_argument("--gemv-ar", action="store_true", help="fused GEMV + AllReduce (Sec. III-B), several shapes")
     ap.add_argument("--gemv-m", type=int, default=0, help="with --gemv-ar: only the shape with this M")
+    ap.add_argument("--backward", action="store_true", help="embedding backward fused with the gradient's arrival")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -615,6 +687,10 @@ def main():
         return 0
     if a.row_probe:
         run_row_probe()
+        return 0
+    if a.backward:
+        for n in (["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
+            run_backward(n, a.steps, a.warmup)
         return 0
     if a.gemv_ar:
         shapes = [sh for sh in GEMV_SHAPES if a.gemv_m in (0, sh[0])]

@@ -174,6 +174,42 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
                      int32_t R, uint32_t expected_epoch, hipStream_t stream);
 
 /*
+ * Embedding backward fused with the arrival of the gradient All-to-All (the
+ * paper overlaps the backward embedding operations with their All-to-All as
+ * well, Sec. IV-D).  The table owner receives the gradient of every pooled
+ * vector of the batch in the send layout of the forward:
+ *   grad_buf: device fp32 [B * sum(D)], pooled vector (t, b) at
+ *     grad_buf[b * sum(D) + off_t ..] (the [R][B/R][sum D] order).
+ *   grad_flags: NULL -- the gradient is complete (bulk-synchronous: launch
+ *     after the collective); or the per-slice epoch flags of the gradient's
+ *     arrival (same layout as the forward's flags for this plan's
+ *     slice_granule): the runs of a slice start once its flag reaches
+ *     expected_epoch (bounded by consume_timeout_us; a timeout is reported
+ *     by ebag_a2a_status and leaves that run's rows unwritten).
+ *   offsets, weights: the forward's bags (weights NULL for plain or mean
+ *     pooling; the plan's pooling_mode applies).
+ *   values: device fp32 output, one row per lookup: for each table t, in
+ *     lookup order, nnz_t = offsets[(t+1)B] - offsets[tB] rows of D_t floats;
+ *     table blocks follow each other in table order.  Lookup k of bag (t, b)
+ *     gets w_k * grad (sum; w_k = 1 without weights) or grad / L (mean), each
+ *     value rounded once to fp32 -- the values of the sparse gradient of an
+ *     EmbeddingBag, whose indices are the forward's indices.
+ */
+int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_flags, uint32_t expected_epoch,
+                      const int64_t* offsets, const float* weights, int64_t B, int32_t R, float* values,
+                      hipStream_t stream);
+
+/*
+ * One-GPU stand-in for the arrival of an All-to-All: copies every slice of
+ * src into dst (same layout, [B * sum(D)] fp32) in slice order and, once a
+ * slice is stored (device-scope stores), adds 1 to its flag in flags (the
+ * layout of the forward's flags for this plan).  Used to feed
+ * ebag_a2a_backward from a second stream.
+ */
+int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags, int64_t B, int32_t R,
+                     hipStream_t stream);
+
+/*
  * Synchronise the device and read the plan's status word.
  *   timed_out: 1 if a consumer gave up waiting, else 0.
  *   first_missing_flag: lowest flag index a consumer timed out on, else -1.

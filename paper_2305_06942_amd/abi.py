@@ -66,6 +66,8 @@ _SIGS = {
     "ebag_a2a_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_unfused_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_consume": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, _P], ctypes.c_int),
+    "ebag_a2a_backward": ([_P, _P, _P, ctypes.c_uint32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P], ctypes.c_int),
+    "ebag_a2a_deliver": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P], ctypes.c_int),
     "ebag_a2a_status": ([_P, _P, _P], ctypes.c_int),
     "ebag_a2a_status_ex": ([_P, _P], ctypes.c_int),
     "ebag_a2a_reset": ([_P], ctypes.c_int),
@@ -191,6 +193,15 @@ class Plan:
     def consume(self, send, flags, recv, B, R, expected_epoch, stream=None):
         _check(self._lib.ebag_a2a_consume(self._h, _addr(send), _addr(flags), _addr(recv), int(B), int(R),
                                           int(expected_epoch) & 0xFFFFFFFF, _stream(stream)))
+
+    def backward(self, grad, offsets, weights, B, R, values, grad_flags=None, expected_epoch=0, stream=None):
+        _check(self._lib.ebag_a2a_backward(self._h, _addr(grad), _addr(grad_flags), int(expected_epoch) & 0xFFFFFFFF,
+                                           _addr(offsets), _addr(weights), int(B), int(R), _addr(values),
+                                           _stream(stream)))
+
+    def deliver(self, src, dst, flags, B, R, stream=None):
+        _check(self._lib.ebag_a2a_deliver(self._h, _addr(src), _addr(dst), _addr(flags), int(B), int(R),
+                                          _stream(stream)))
 
     def status(self):
         """(timed_out, first_missing_flag); synchronises the device."""

@@ -1,0 +1,195 @@
+// Embedding backward fused with the arrival of the gradient All-to-All, and
+// the one-GPU stand-in for that arrival (the deliver kernel).
+//
+// The table owner receives the gradient of every pooled vector in the
+// destination-partitioned layout grad[R][S][sum D] (= [B][sum D]), slice by
+// slice.  The gradient of lookup k of bag (t, b) is w_k * grad[b][off_t ..
+// off_t + D_t) (sum mode; w_k = 1 without weights) or grad[b][...] / L (mean
+// mode).  Output: per table, in lookup order, nnz_t rows of D_t fp32 values;
+// table blocks follow each other in table order.
+//
+// Runs are the forward's: up to K consecutive samples of one table inside
+// one slice, numbered slice-major.  With flags, a workgroup waits for its
+// slice's flag before touching the gradient, so slices are expanded as they
+// arrive.  Each wave scales its bag's gradient row once into LDS (the mean's
+// division happens there, once per element), then writes the bag's L output
+// rows -- one contiguous block of L * D_t floats -- with 16-byte stores.
+#include "common.h"
+
+namespace ebag {
+namespace {
+
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+template <class T>
+__device__ __forceinline__ T sld(const T* p, int64_t i) {
+  return ((const __attribute__((address_space(4))) T*)p)[i];
+}
+
+// First float of every table's output block: base[t] = sum over t' < t of
+// nnz_t' * D_t' (one thread; T is small).
+__global__ void value_base_kernel(const int64_t* offsets, const TabMeta* meta, int32_t T, int64_t B,
+                                  int64_t* base) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  int64_t acc = 0;
+  for (int32_t t = 0; t < T; ++t) {
+    base[t] = acc;
+    acc += (offsets[(int64_t)(t + 1) * B] - offsets[(int64_t)t * B]) * meta[t].dim;
+  }
+  base[T] = acc;
+}
+
+__global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
+  extern __shared__ float s_row[];   // [waves][max_dim]: each wave's scaled gradient row
+  __shared__ int s_bad;
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int W = blockDim.x >> 6;
+  const int64_t per_slice = (int64_t)a.T * a.J;
+  const int64_t q = blockIdx.x;
+  const int64_t gs = q / per_slice;
+  const int64_t rem = q - gs * per_slice;
+  const int tpos = (int)(rem % a.T);
+  const int j = (int)(rem / a.T);
+  const int t = sld(a.tperm, tpos);
+  const int64_t g = slice_at(a.so, gs);
+  if (a.flags) {
+    if (threadIdx.x == 0) {
+      const int64_t f = a.per_table ? g * a.T + t : g;
+      const uint64_t t0 = wall_clock64();
+      int bad = 0;
+      while ((int32_t)(__hip_atomic_load(&a.flags[f], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - a.epoch) < 0) {
+        if (wall_clock64() - t0 > a.timeout_ticks) {
+          __hip_atomic_store(&a.status[ST_TIMED_OUT], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          atomicMin(&a.status[ST_FIRST_MISSING], (int32_t)f);
+          bad = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(4);
+      }
+      s_bad = bad;
+    }
+    __syncthreads();
+    if (s_bad) return;
+  }
+  const int dim = sld(&a.meta[t].dim, 0);
+  const int col_off = sld(&a.meta[t].col_off, 0);
+  const int V = dim >> 2;  // float4 per row
+  const int64_t b0 = g * a.C + (int64_t)j * a.K;
+  const int64_t b1 = min(b0 + (int64_t)a.K, (g + 1) * (int64_t)a.C);
+  const int64_t nb = b1 - b0;
+  const int64_t per = (nb + W - 1) / W;
+  const int64_t bb = b0 + wid * per;
+  const int64_t be = min(bb + per, b1);
+  const int64_t obase = (int64_t)t * a.B;
+  const int64_t first = sld(a.offsets, obase);
+  const int64_t vbase = sld(a.value_base, t);
+  float* srow = s_row + wid * a.max_dim;
+  for (int64_t b = bb; b < be; ++b) {
+    const int64_t lo = sld(a.offsets, obase + b), hi = sld(a.offsets, obase + b + 1);
+    const int64_t L = hi - lo;
+    if (L <= 0) continue;
+    // the bag's gradient row, scaled once (device-scope loads: with flags the
+    // row was stored by another kernel that is still running)
+    const float* grow = a.grad + b * a.sum_dim + col_off;
+    for (int e = lane; e < dim; e += 64) {
+      float v = a.flags ? __hip_atomic_load(const_cast<float*>(grow + e), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                        : grow[e];
+      if (a.mean) v = v / (float)L;
+      srow[e] = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // L rows of D floats, contiguous: float4 element e is row e / V, vector e % V
+    float4* out = reinterpret_cast<float4*>(a.values + vbase + (lo - first) * dim);
+    const float4* s4 = reinterpret_cast<const float4*>(srow);
+    const int64_t n = L * V;
+    for (int64_t e = lane; e < n; e += 64) {
+      const int64_t k = e / V;
+      float4 x = s4[e - k * V];
+      if (a.weights) {
+        const float w = a.weights[lo + k];
+        x = make_float4(w * x.x, w * x.y, w * x.z, w * x.w);
+      }
+      out[e] = x;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+// One-GPU stand-in for the gradient All-to-All's arrival: single-wave
+// workgroups copy work items (32 KiB pieces of a whole slice, or one
+// (slice, table) block per item with per-table slices) from src to dst in
+// slice order with device-scope stores; when the last piece of a slice is
+// stored, its flag is incremented.
+__global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
+  const int lane = threadIdx.x;
+  const int64_t per_slice = a.per_table ? a.T : a.pieces;
+  const int64_t n_items = a.so.n_chunks * per_slice;
+  for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
+    const int64_t gs = x / per_slice;
+    const int64_t p = x - gs * per_slice;
+    const int64_t g = slice_at(a.so, gs);
+    if (a.per_table) {
+      const int t = __builtin_amdgcn_readfirstlane(a.tperm[p]);
+      const int dim = __builtin_amdgcn_readfirstlane(a.meta[t].dim);
+      const int col_off = __builtin_amdgcn_readfirstlane(a.meta[t].col_off);
+      const int v4 = dim >> 2, ld4 = a.sum_dim >> 2;
+      const int64_t base = g * a.chunk_floats + col_off;
+      const float4* src = reinterpret_cast<const float4*>(a.src + base);
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          a.dst + base, 0, ((a.C - 1) * a.sum_dim + dim) * 4, 0x00020000);
+      for (int e = lane; e < a.C * v4; e += 64) {
+        const int row = e / v4;
+        const int off = row * ld4 + (e - row * v4);
+        const float4 v = src[off];
+        const u4v u = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
+        __builtin_amdgcn_raw_buffer_store_b128(u, rs, off * 16, 0, 16);  // device-scope store
+      }
+      wait_all_memory();
+      if (lane == 0)
+        __hip_atomic_fetch_add(&a.flags[g * a.T + t], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      const int64_t chunk_f4 = a.chunk_floats >> 2;
+      const int64_t e0 = p * a.piece_f4;
+      const int n = (int)min(a.piece_f4, chunk_f4 - e0);
+      const float4* src = reinterpret_cast<const float4*>(a.src + g * a.chunk_floats) + e0;
+      float4* dst = reinterpret_cast<float4*>(a.dst + g * a.chunk_floats) + e0;
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, n * 16, 0x00020000);
+      for (int i = lane; i < n; i += 64) {
+        const float4 v = src[i];
+        const u4v u = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
+        __builtin_amdgcn_raw_buffer_store_b128(u, rs, i * 16, 0, 16);  // device-scope store
+      }
+      wait_all_memory();
+      if (lane == 0 &&
+          __hip_atomic_fetch_add(&a.counters[g], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              (uint32_t)a.pieces - 1) {
+        __hip_atomic_store(&a.counters[g], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&a.flags[g], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_backward(const BackwardArgs& a, int64_t* value_base, int block, size_t lds, hipStream_t stream) {
+  hipLaunchKernelGGL(value_base_kernel, dim3(1), dim3(64), 0, stream, a.offsets, a.meta, a.T, a.B, value_base);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(backward_kernel, dim3((unsigned)a.nruns), dim3(block), lds, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_deliver(const DeliverArgs& a, int grid, hipStream_t stream) {
+  hipLaunchKernelGGL(deliver_kernel, dim3(grid), dim3(64), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace ebag

@@ -138,6 +138,8 @@ struct ebag_a2a_plan {
   float* d_scratch = nullptr;
   int32_t* d_status = nullptr;
   uint32_t* d_ticket = nullptr;  // persistent-grid run ticket [2], self-resetting
+  int64_t* d_value_base = nullptr;    // backward: first float of each table's block [T + 1]
+  uint32_t* d_deliver_cnt = nullptr;  // deliver: pieces stored per slice [max_chunks], self-resetting
   uint64_t* d_trace_release = nullptr;
   uint64_t* d_trace_drain = nullptr;
 };
@@ -155,6 +157,8 @@ void free_plan(ebag_a2a_plan* h) {
   (void)hipFree(h->d_scratch);
   (void)hipFree(h->d_status);
   (void)hipFree(h->d_ticket);
+  (void)hipFree(h->d_value_base);
+  (void)hipFree(h->d_deliver_cnt);
   (void)hipFree(h->d_trace_release);
   (void)hipFree(h->d_trace_drain);
   delete h;
@@ -174,6 +178,25 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
   if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
+  return EBAG_OK;
+}
+
+// B / R checks shared by every entry point that walks slices; fills the
+// slice order.
+int check_split(const ebag_a2a_plan* h, int64_t B, int32_t R, SliceOrder* so) {
+  if (B <= 0 || R <= 0) return fail(EBAG_EINVAL, "B and R must be positive (B=%lld R=%d)", (long long)B, R);
+  if (B > h->max_batch) return fail(EBAG_EINVAL, "B=%lld exceeds max_batch=%lld", (long long)B, (long long)h->max_batch);
+  if (R > h->max_ranks) return fail(EBAG_EINVAL, "R=%d exceeds max_ranks=%d", R, h->max_ranks);
+  if (B % R != 0) return fail(EBAG_EINVAL, "B=%lld is not a multiple of R=%d", (long long)B, R);
+  if ((B / R) % h->C != 0)
+    return fail(EBAG_EINVAL, "B/R=%lld is not a multiple of chunk_samples=%d", (long long)(B / R), h->C);
+  if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
+    return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
+  so->n_chunks = B / h->C;
+  so->per_rank = (B / R) / h->C;
+  so->self = h->opts.self_rank;
+  so->order = h->opts.chunk_order;
+  so->pad = 0;
   return EBAG_OK;
 }
 
@@ -391,6 +414,9 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   CREATE_TRY(hipMalloc((void**)&h->d_counters, sizeof(uint32_t) * h->max_flags), "alloc slice counters");
   CREATE_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero slice counters");
   CREATE_TRY(hipMalloc((void**)&h->d_scratch, sizeof(float) * (size_t)max_batch * (size_t)sum_dim), "alloc scratch");
+  CREATE_TRY(hipMalloc((void**)&h->d_value_base, sizeof(int64_t) * (num_tables + 1)), "alloc value bases");
+  CREATE_TRY(hipMalloc((void**)&h->d_deliver_cnt, sizeof(uint32_t) * h->max_chunks), "alloc deliver counters");
+  CREATE_TRY(hipMemset(h->d_deliver_cnt, 0, sizeof(uint32_t) * h->max_chunks), "zero deliver counters");
   CREATE_TRY(hipMalloc((void**)&h->d_ticket, 2 * sizeof(uint32_t)), "alloc run ticket");
   CREATE_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
   CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
@@ -509,6 +535,84 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   return EBAG_OK;
 }
 
+int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_flags, uint32_t expected_epoch,
+                      const int64_t* offsets, const float* weights, int64_t B, int32_t R, float* values,
+                      hipStream_t stream) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (!grad_buf || !offsets || !values) return fail(EBAG_EINVAL, "null grad_buf, offsets or values");
+  if (!aligned16(grad_buf) || !aligned16(values)) return fail(EBAG_EINVAL, "grad_buf or values not 16-byte aligned");
+  if (weights && h->opts.pooling_mode == 1) return fail(EBAG_EINVAL, "mean pooling takes no weights");
+  SliceOrder so;
+  int rc = check_split(h, B, R, &so);
+  if (rc) return rc;
+  int32_t max_dim = 0;
+  for (const TabMeta& m : h->meta) max_dim = m.dim > max_dim ? m.dim : max_dim;
+  const int block = 64 * h->opts.waves_per_wg;
+  const size_t lds = (size_t)h->opts.waves_per_wg * max_dim * sizeof(float);
+  if (lds > 65536) return fail(EBAG_EUNSUPPORTED, "backward: waves_per_wg x widest row (%zu bytes) above 64 KiB", lds);
+  BackwardArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.grad = grad_buf;
+  a.flags = grad_flags;
+  a.values = values;
+  a.offsets = offsets;
+  a.weights = weights;
+  a.meta = h->d_meta;
+  a.tperm = h->d_tperm;
+  a.value_base = h->d_value_base;
+  a.status = h->d_status;
+  a.B = B;
+  a.timeout_ticks = (uint64_t)((double)h->opts.consume_timeout_us * h->ticks_per_us);
+  a.so = so;
+  a.T = h->T;
+  a.C = h->C;
+  a.K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  a.J = (h->C + a.K - 1) / a.K;
+  a.nruns = so.n_chunks * (int64_t)h->T * a.J;
+  if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
+  a.sum_dim = h->sum_dim;
+  a.max_dim = max_dim;
+  a.per_table = h->opts.slice_granule == 1;
+  a.mean = h->opts.pooling_mode == 1;
+  a.epoch = expected_epoch;
+  const hipError_t e = launch_backward(a, h->d_value_base, block, lds, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch backward kernels");
+  return EBAG_OK;
+}
+
+int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags, int64_t B, int32_t R,
+                     hipStream_t stream) {
+  if (!h) return fail(EBAG_EINVAL, "null plan");
+  if (!src || !dst || !flags) return fail(EBAG_EINVAL, "null src, dst or flags");
+  if (!aligned16(src) || !aligned16(dst)) return fail(EBAG_EINVAL, "src or dst not 16-byte aligned");
+  SliceOrder so;
+  int rc = check_split(h, B, R, &so);
+  if (rc) return rc;
+  DeliverArgs d;
+  std::memset(&d, 0, sizeof d);
+  d.src = src;
+  d.dst = dst;
+  d.flags = flags;
+  d.counters = h->d_deliver_cnt;
+  d.meta = h->d_meta;
+  d.tperm = h->d_tperm;
+  d.chunk_floats = (int64_t)h->C * h->sum_dim;
+  const int64_t chunk_f4 = d.chunk_floats / 4;
+  d.piece_f4 = chunk_f4 < 2048 ? chunk_f4 : 2048;
+  d.pieces = (chunk_f4 + d.piece_f4 - 1) / d.piece_f4;
+  d.so = so;
+  d.T = h->T;
+  d.C = h->C;
+  d.sum_dim = h->sum_dim;
+  d.per_table = h->opts.slice_granule == 1;
+  const int64_t items = so.n_chunks * (d.per_table ? h->T : d.pieces);
+  int64_t grid = h->opts.consumer_wgs;
+  if (grid > items) grid = items;
+  const hipError_t e = launch_deliver(d, (int)grid, stream);
+  if (e != hipSuccess) return hip_fail(e, "launch deliver kernel");
+  return EBAG_OK;
+}
+
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]) {
   if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
@@ -535,6 +639,7 @@ int ebag_a2a_reset(ebag_a2a_t h) {
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero counters");
   HIP_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
+  HIP_TRY(hipMemset(h->d_deliver_cnt, 0, sizeof(uint32_t) * h->max_chunks), "zero deliver counters");
   HIP_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "reset status");
   if (h->d_trace_release) {
     HIP_TRY(hipMemset(h->d_trace_release, 0, sizeof(uint64_t) * h->max_flags), "zero trace");

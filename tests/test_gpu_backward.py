@@ -1,0 +1,162 @@
+"""Embedding backward (per-lookup gradient rows) through the C ABI against the
+oracle, bulk-synchronous and fused with the gradient's arrival.  Every value
+is one fp32 multiply or divide of a received gradient value, so GPU and
+oracle agree bit for bit."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import device as sdev
+from tests.gpu_util import make_plan, say
+from tests.test_gpu_parity import EDGE, SMALL, _custom_inputs
+
+pytestmark = pytest.mark.gpu
+
+_QUEUES = []
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _queues():
+    import paper_2305_06942_amd as ebag
+    if not _QUEUES:
+        _QUEUES.extend([ebag.queue_stream(), ebag.queue_stream()])
+    return _QUEUES
+
+
+def _grad(w, seed):
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    return torch.randn((w.B, w.sum_dim), generator=g, device="cuda")
+
+
+def _n_values(inp):
+    w = inp.w
+    return int(sum((inp.offsets[(t + 1) * w.B] - inp.offsets[t * w.B]) * w.dims[t] for t in range(w.T)))
+
+
+def _expected(inp, grad, mean):
+    return oracle.backward(inp.w.dims, inp.offsets, inp.weights, grad.cpu().numpy(), inp.w.B, inp.w.R, mean=mean)
+
+
+def _check(inp, grad, values, mean):
+    want = _expected(inp, grad, mean)
+    got = values.cpu().numpy()
+    bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+    assert bad.size == 0, f"{bad.size} values differ, first at {bad[0]}: gpu {got[bad[0]]} oracle {want[bad[0]]}"
+
+
+def _unweighted(inp):
+    return dataclasses.replace(inp, w=inp.w.with_(weighted=False), weights=None)
+
+
+@pytest.mark.parametrize("granule", [0, 1])
+@pytest.mark.parametrize("mean", [False, True])
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_backward_bulk_synchronous(name, mean, granule):
+    import torch
+    inp = synth.make_inputs(SMALL[name])
+    if mean:
+        inp = _unweighted(inp)
+    w = inp.w
+    dev = sdev.to_device(inp)
+    grad = _grad(w, 5)
+    plan = make_plan(w, pooling_mode=int(mean), slice_granule=granule)
+    values = torch.full((_n_values(inp),), float("nan"), device="cuda")
+    plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
+    torch.cuda.synchronize()
+    _check(inp, grad, values, mean)
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_backward_edge_cases(name):
+    import torch
+    inp = _custom_inputs(*EDGE[name], seed=len(name))
+    w = inp.w
+    dev = sdev.to_device(inp)
+    grad = _grad(w, 9)
+    plan = make_plan(w)
+    values = torch.full((max(_n_values(inp), 1),), float("nan"), device="cuda")
+    plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
+    torch.cuda.synchronize()
+    _check(inp, grad, values[:_n_values(inp)], False)
+
+
+def _fused(plan, w, dev, grad_dp, grad_recv, flags, values, epoch):
+    import torch
+    main = torch.cuda.current_stream()
+    send_q, bwd_q = _queues()
+    send_q.wait_stream(main)
+    bwd_q.wait_stream(main)
+    with torch.cuda.stream(send_q):  # the gradient arriving, slice by slice
+        plan.deliver(grad_dp, grad_recv, flags, w.B, w.R)
+    with torch.cuda.stream(bwd_q):   # expanded as it arrives
+        plan.backward(grad_recv, dev.offsets, dev.weights, w.B, w.R, values, grad_flags=flags, expected_epoch=epoch)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("opts", [dict(), dict(slice_granule=1), dict(chunk_order=1, self_rank=1),
+                                  dict(pooling_mode=1)], ids=lambda o: ",".join(f"{k}={v}" for k, v in o.items()) or "default")
+def test_backward_fused_with_delivery(opts):
+    import torch
+    inp = synth.make_inputs(SMALL["mixed_small"])
+    if opts.get("pooling_mode"):
+        inp = _unweighted(inp)
+    w = inp.w
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, **opts)
+    per_slice = w.T if opts.get("slice_granule") else 1
+    flags = torch.zeros(w.n_chunks * per_slice, dtype=torch.int32, device="cuda")
+    grad_recv = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+    for epoch in (1, 2, 3):
+        grad_dp = _grad(w, 100 + epoch)
+        values = torch.full((_n_values(inp),), float("nan"), device="cuda")
+        _fused(plan, w, dev, grad_dp, grad_recv, flags, values, epoch)
+        assert plan.status_ex() == (0, -1, 0, -1)
+        assert np.all(flags.cpu().numpy() == epoch)
+        assert torch.equal(grad_dp, grad_recv)
+        _check(inp, grad_dp, values, bool(opts.get("pooling_mode")))
+
+
+def test_backward_times_out_without_delivery():
+    import torch
+    w = SMALL["dlrm_small"]
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, consume_timeout_us=20000)
+    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    values = torch.full((_n_values(inp),), float("nan"), device="cuda")
+    plan.backward(_grad(w, 1), dev.offsets, dev.weights, w.B, w.R, values, grad_flags=flags, expected_epoch=1)
+    timed_out, missing = plan.status()
+    assert timed_out == 1 and missing == 0
+    plan.reset()
+    assert torch.isnan(values).all()
+
+
+def test_backward_full_size_dlrm_fused():
+    """dlrm size: every value of the fused delivery + backward, bit for bit."""
+    import torch
+    w = synth.FULL["dlrm"]
+    say("backward full dlrm")
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    grad_recv = torch.empty((w.B, w.sum_dim), device="cuda")
+    grad_dp = _grad(w, 7)
+    values = torch.full((_n_values(inp),), float("nan"), device="cuda")
+    _fused(plan, w, dev, grad_dp, grad_recv, flags, values, 1)
+    assert plan.status_ex() == (0, -1, 0, -1)
+    _check(inp, grad_dp, values, False)
+    del values
+    torch.cuda.empty_cache()
