@@ -25,8 +25,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public specification
-KERNEL_SOURCES = ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
-                  "paper_2305_06942_amd/csrc/repack_consume.hip"]
+# Sources whose text fixes each profiled kernel: committed counter records
+# are used only while the hash of these files is unchanged.
+KERNEL_SOURCES = {
+    "fused_pool_kernel": ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
+                          "paper_2305_06942_amd/csrc/repack_consume.hip"],
+    "backward_kernel": ["paper_2305_06942_amd/csrc/backward.hip", "paper_2305_06942_amd/csrc/common.h"],
+}
+TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json"}
 # Plan options per workload.  Only the row-cache policy differs: workloads
 # whose indices follow a skewed (Zipf) law re-read hot rows, so their table
 # rows are read through the caches; uniform workloads stream rows (default).
@@ -45,9 +51,9 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_hash():
+def kernel_hash(kernel="fused_pool_kernel"):
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -65,15 +71,15 @@ def algorithmic_bytes(w, lengths, weighted, n_flags=None):
     return rows + 4 * nnz + (4 * nnz if weighted else 0) + 8 * (w.T * w.B + 1) + 4 * w.B * w.sum_dim + 4 * n_flags
 
 
-def traffic_record(workload):
+def traffic_record(workload, kernel="fused_pool_kernel"):
     """HBM bytes per launch from committed rocprofv3 counter runs, only if the
     kernel sources have not changed since they were taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    path = os.path.join(ROOT, "profiles", TRAFFIC_FILE[kernel].format(workload))
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_hash") != kernel_hash():
+    if rec.get("kernel_hash") != kernel_hash(kernel):
         return None
     return rec
 
@@ -450,10 +456,12 @@ def backward_bytes(w, lengths, weighted):
     return rows + 4 * w.B * w.sum_dim + 8 * (w.T * w.B + 1) + (4 * nnz if weighted else 0)
 
 
-def run_backward(name, steps, warmup):
+def run_backward(name, steps, warmup, profile=False):
     """Embedding backward: the kernel alone (gradient complete), the
     bulk-synchronous sequence (delivery of the gradient, then the backward)
-    and the fused one (backward expanding slices as the delivery lands)."""
+    and the fused one (backward expanding slices as the delivery lands).
+    profile: the kernel alone and the delivery, on one ordinary stream (for
+    rocprofv3 kernel traces)."""
     import torch
     import paper_2305_06942_amd as ebag
     w, inp, dev, _, _ = _setup(name)
@@ -473,6 +481,19 @@ def run_backward(name, steps, warmup):
     for _ in range(warmup):
         bwd()
     k_ms = time_launches(bwd, steps, s)
+    if profile:
+        d_ms = time_launches(lambda: plan.deliver(grad_dp, grad_recv, flags, w.B, w.R), steps, s)
+        from synth import device as _sd
+        src = torch.ones((1 << 30) // 4, device="cuda")  # counter calibration: two 1 GiB copies
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            _sd.copy(dst, src, 1 << 30)
+        torch.cuda.synchronize()
+        print(json.dumps({"operator": "embedding_backward", "workload": name, "kernel_us": round(k_ms * 1e3, 2),
+                          "deliver_us": round(d_ms * 1e3, 2), "algorithmic_bytes": nbytes,
+                          "calibration_copy_bytes": 1 << 30}), flush=True)
+        plan.close()
+        return None
     epoch = [0]
     send_q, bwd_q = ebag.queue_stream(), ebag.queue_stream()
 
@@ -500,16 +521,43 @@ def run_backward(name, steps, warmup):
         return sorted(times)[len(times) // 2]
     f_ms = sequence(True)
     u_ms = sequence(False)
+    tr = traffic_record(name, "backward_kernel")
     row = {"operator": "embedding_backward", "workload": name, "values_bytes": 4 * n_vals,
            "algorithmic_bytes": nbytes, "kernel_us": round(k_ms * 1e3, 2),
            "fused_with_delivery_us": round(f_ms * 1e3, 2), "delivery_then_backward_us": round(u_ms * 1e3, 2),
            "fused_speedup": round(u_ms / f_ms, 4),
            "roofline": {"bound": "hbm", "achieved": round(nbytes / (k_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                        "unit": "GB/s", "frac": round(nbytes / (k_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+                        "unit": "GB/s", "frac": round(nbytes / (k_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        "traffic": tr["hbm_bytes_per_launch"] if tr else None},
            "data": "synthetic: the workload's bags, a seeded torch.randn pooled gradient"}
     print(json.dumps(row), flush=True)
     plan.close()
     return row
+
+
+def run_backward_sweep(name, steps, warmup):
+    """Backward kernel time over its launch shape: bags and waves per
+    workgroup (the gradient complete; one JSON line per shape)."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    w, inp, dev, _, _ = _setup(name)
+    n_vals = int(sum((inp.offsets[(t + 1) * w.B] - inp.offsets[t * w.B]) * w.dims[t] for t in range(w.T)))
+    values = torch.empty((n_vals,), device="cuda")
+    grad = torch.randn((w.B, w.sum_dim), generator=torch.Generator(device="cuda").manual_seed(2305), device="cuda")
+    nbytes = backward_bytes(w, inp.lengths, inp.weights is not None)
+    s = torch.cuda.current_stream()
+    for waves in (4, 8, 16):
+        for bags in (1, 2, 3, 4, 8, 16):
+            plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, backward_waves_per_wg=waves,
+                             backward_bags_per_run=bags)
+            f = lambda: plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
+            for _ in range(warmup):
+                f()
+            ms = time_launches(f, steps, s)
+            print(json.dumps({"operator": "embedding_backward", "workload": name, "waves_per_wg": waves,
+                              "bags_per_wg": bags, "kernel_us": round(ms * 1e3, 1),
+                              "GB/s": round(nbytes / ms / 1e6, 1)}), flush=True)
+            plan.close()
 
 
 GEMV_SHAPES = [(16384, 8192), (32768, 8192), (65536, 8192)]  # (M outputs, K total), R = 4 ranks, fp16
@@ -638,7 +686,7 @@ def traffic(fetch_dir, write_dir, workload, kernel="fused_pool_kernel", calib="c
     w_scale = (nb / 1024.0) / wr[cw]
     fetch_b = fe[kf] * f_scale * 1024
     write_b = wr[kw] * w_scale * 1024
-    return {"workload": workload, "kernel": kernel, "kernel_hash": kernel_hash(),
+    return {"workload": workload, "kernel": kernel, "kernel_hash": kernel_hash(kernel),
             "fetch_kib_raw": fe[kf], "write_kib_raw": wr[kw], "fetch_scale": round(f_scale, 4),
             "write_scale": round(w_scale, 4), "fetch_bytes": int(fetch_b), "write_bytes": int(write_b),
             "hbm_bytes_per_launch": int(fetch_b + write_b)}
@@ -663,12 +711,14 @@ def main():
     ap.add_argument("--gemv-ar", action="store_true", help="fused GEMV + AllReduce (Sec. III-B), several shapes")
     ap.add_argument("--gemv-m", type=int, default=0, help="with --gemv-ar: only the shape with this M")
     ap.add_argument("--backward", action="store_true", help="embedding backward fused with the gradient's arrival")
+    ap.add_argument("--backward-sweep", action="store_true", help="backward kernel time per launch shape")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
         return 0
     if a.traffic:
-        print(json.dumps(traffic(a.traffic[0], a.traffic[1], a.workload), indent=1))
+        kernel = "backward_kernel" if a.backward else "fused_pool_kernel"
+        print(json.dumps(traffic(a.traffic[0], a.traffic[1], a.workload, kernel=kernel), indent=1))
         return 0
     if a.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
@@ -688,9 +738,13 @@ def main():
     if a.row_probe:
         run_row_probe()
         return 0
+    if a.backward_sweep:
+        for n in (["dlrm", "large", "mixed"] if a.all else [a.workload]):
+            run_backward_sweep(n, a.steps, a.warmup)
+        return 0
     if a.backward:
         for n in (["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
-            run_backward(n, a.steps, a.warmup)
+            run_backward(n, a.steps, a.warmup, profile=a.profile)
         return 0
     if a.gemv_ar:
         shapes = [sh for sh in GEMV_SHAPES if a.gemv_m in (0, sh[0])]

@@ -35,6 +35,8 @@ class Opts(ctypes.Structure):
         ("consume_timeout_us", ctypes.c_int64),
         ("pooling_mode", ctypes.c_int32),
         ("slice_granule", ctypes.c_int32),
+        ("backward_bags_per_run", ctypes.c_int32),
+        ("backward_waves_per_wg", ctypes.c_int32),
     ]
 
 

@@ -11,15 +11,18 @@
 // Runs are the forward's: up to K consecutive samples of one table inside
 // one slice, numbered slice-major.  With flags, a workgroup waits for its
 // slice's flag before touching the gradient, so slices are expanded as they
-// arrive.  Each wave scales its bag's gradient row once into LDS (the mean's
-// division happens there, once per element), then writes the bag's L output
-// rows -- one contiguous block of L * D_t floats -- with 16-byte stores.
+// arrive.  The workgroup scales its K gradient rows once into LDS (the
+// mean's division happens there, once per element); the run's output rows
+// are contiguous (consecutive bags' lookups follow each other), so the whole
+// workgroup writes them as one block with 16-byte non-temporal stores,
+// balanced however the bag lengths vary.
 #include "common.h"
 
 namespace ebag {
 namespace {
 
 typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+typedef float f4v __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void wait_all_memory() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -29,24 +32,38 @@ __device__ __forceinline__ T sld(const T* p, int64_t i) {
 }
 
 // First float of every table's output block: base[t] = sum over t' < t of
-// nnz_t' * D_t' (one thread; T is small).
-__global__ void value_base_kernel(const int64_t* offsets, const TabMeta* meta, int32_t T, int64_t B,
-                                  int64_t* base) {
-  if (blockIdx.x != 0 || threadIdx.x != 0) return;
-  int64_t acc = 0;
-  for (int32_t t = 0; t < T; ++t) {
-    base[t] = acc;
-    acc += (offsets[(int64_t)(t + 1) * B] - offsets[(int64_t)t * B]) * meta[t].dim;
+// nnz_t' * D_t', base[T] the total.  One workgroup of 256 threads: the
+// tables' sizes are loaded 256 at a time (independent loads, one memory
+// latency per 256 tables) and prefix-summed in LDS.
+__global__ __launch_bounds__(256) void value_base_kernel(const int64_t* offsets, const TabMeta* meta, int32_t T,
+                                                         int64_t B, int64_t* base) {
+  __shared__ int64_t s_scan[256];
+  const int tid = threadIdx.x;
+  int64_t carry = 0;
+  for (int32_t c0 = 0; c0 < T; c0 += 256) {
+    const int32_t t = c0 + tid;
+    const int64_t v = t < T ? (offsets[(int64_t)(t + 1) * B] - offsets[(int64_t)t * B]) * meta[t].dim : 0;
+    s_scan[tid] = v;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {  // inclusive Hillis-Steele scan
+      const int64_t add = tid >= d ? s_scan[tid - d] : 0;
+      __syncthreads();
+      s_scan[tid] += add;
+      __syncthreads();
+    }
+    if (t < T) base[t] = carry + s_scan[tid] - v;
+    carry += s_scan[255];
+    __syncthreads();
   }
-  base[T] = acc;
+  if (tid == 0) base[T] = carry;
 }
 
 __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
-  extern __shared__ float s_row[];   // [waves][max_dim]: each wave's scaled gradient row
+  // LDS: the run's K scaled gradient rows [K][dim], then its K + 1 bag
+  // offsets relative to the run's first lookup.
+  extern __shared__ f4v s_lds[];
   __shared__ int s_bad;
-  const int lane = threadIdx.x & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int W = blockDim.x >> 6;
+  const int tid = threadIdx.x;
   const int64_t per_slice = (int64_t)a.T * a.J;
   const int64_t q = blockIdx.x;
   const int64_t gs = q / per_slice;
@@ -56,7 +73,7 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   const int t = sld(a.tperm, tpos);
   const int64_t g = slice_at(a.so, gs);
   if (a.flags) {
-    if (threadIdx.x == 0) {
+    if (tid == 0) {
       const int64_t f = a.per_table ? g * a.T + t : g;
       const uint64_t t0 = wall_clock64();
       int bad = 0;
@@ -78,47 +95,50 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   const int col_off = sld(&a.meta[t].col_off, 0);
   const int V = dim >> 2;  // float4 per row
   const int64_t b0 = g * a.C + (int64_t)j * a.K;
-  const int64_t b1 = min(b0 + (int64_t)a.K, (g + 1) * (int64_t)a.C);
-  const int64_t nb = b1 - b0;
-  const int64_t per = (nb + W - 1) / W;
-  const int64_t bb = b0 + wid * per;
-  const int64_t be = min(bb + per, b1);
-  const int64_t obase = (int64_t)t * a.B;
-  const int64_t first = sld(a.offsets, obase);
-  const int64_t vbase = sld(a.value_base, t);
-  float* srow = s_row + wid * a.max_dim;
-  for (int64_t b = bb; b < be; ++b) {
-    const int64_t lo = sld(a.offsets, obase + b), hi = sld(a.offsets, obase + b + 1);
-    const int64_t L = hi - lo;
-    if (L <= 0) continue;
-    // the bag's gradient row, scaled once (device-scope loads: with flags the
-    // row was stored by another kernel that is still running)
-    const float* grow = a.grad + b * a.sum_dim + col_off;
-    for (int e = lane; e < dim; e += 64) {
-      float v = a.flags ? __hip_atomic_load(const_cast<float*>(grow + e), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                        : grow[e];
-      if (a.mean) v = v / (float)L;
-      srow[e] = v;
+  const int nb = (int)min((int64_t)a.K, (g + 1) * (int64_t)a.C - b0);
+  const int64_t obase = (int64_t)t * a.B + b0;
+  const int64_t lo0 = sld(a.offsets, obase);
+  int64_t* s_off = reinterpret_cast<int64_t*>(s_lds + (int64_t)a.K * (a.max_dim >> 2));
+  if (tid <= nb) s_off[tid] = a.offsets[obase + tid] - lo0;
+  // the run's gradient rows, scaled once (device-scope loads: with flags the
+  // rows were stored by a kernel that may still be running)
+  float* s_rows = reinterpret_cast<float*>(s_lds);
+  for (int e = tid; e < nb * dim; e += blockDim.x) {
+    const int k = e / dim;
+    const int c = e - k * dim;
+    const float* gp = a.grad + (b0 + k) * a.sum_dim + col_off + c;
+    float v = a.flags ? __hip_atomic_load(const_cast<float*>(gp), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *gp;
+    if (a.mean) {
+      const int64_t L = a.offsets[obase + k + 1] - a.offsets[obase + k];
+      v = v / (float)L;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // L rows of D floats, contiguous: float4 element e is row e / V, vector e % V
-    float4* out = reinterpret_cast<float4*>(a.values + vbase + (lo - first) * dim);
-    const float4* s4 = reinterpret_cast<const float4*>(srow);
-    const int64_t n = L * V;
-    for (int64_t e = lane; e < n; e += 64) {
-      const int64_t k = e / V;
-      float4 x = s4[e - k * V];
-      if (a.weights) {
-        const float w = a.weights[lo + k];
-        x = make_float4(w * x.x, w * x.y, w * x.z, w * x.w);
-      }
-      out[e] = x;
+    s_rows[k * dim + c] = v;
+  }
+  __syncthreads();
+  // The run's output is one contiguous block of (lookups of its bags) x dim
+  // floats; the whole workgroup streams it out.  Each thread walks float4
+  // elements tid, tid + blockDim, ... keeping its (row, vector, bag) position
+  // incrementally: no division inside the loop.
+  const int64_t rows = s_off[nb];
+  const int64_t n = rows * V;
+  f4v* out = reinterpret_cast<f4v*>(a.values + sld(a.value_base, t) + (lo0 - sld(a.offsets, (int64_t)t * a.B)) * dim);
+  const int step = blockDim.x;
+  const int dk = step / V, dc = step - (step / V) * V;
+  int64_t k = tid / V;
+  int c = tid - (tid / V) * V;
+  int bag = 0;
+  const float* wts = a.weights ? a.weights + lo0 : nullptr;
+  for (int64_t e = tid; e < n; e += step) {
+    while (bag < nb - 1 && k >= s_off[bag + 1]) ++bag;
+    f4v x = s_lds[bag * V + c];
+    if (wts) x = wts[k] * x;
+    __builtin_nontemporal_store(x, out + e);
+    k += dk;
+    c += dc;
+    if (c >= V) {
+      c -= V;
+      ++k;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -180,7 +200,7 @@ __global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
 }  // namespace
 
 hipError_t launch_backward(const BackwardArgs& a, int64_t* value_base, int block, size_t lds, hipStream_t stream) {
-  hipLaunchKernelGGL(value_base_kernel, dim3(1), dim3(64), 0, stream, a.offsets, a.meta, a.T, a.B, value_base);
+  hipLaunchKernelGGL(value_base_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.meta, a.T, a.B, value_base);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(backward_kernel, dim3((unsigned)a.nruns), dim3(block), lds, stream, a);

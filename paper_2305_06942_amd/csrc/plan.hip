@@ -178,6 +178,9 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
   if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
+  if (o.backward_bags_per_run < 1) return fail(EBAG_EINVAL, "backward_bags_per_run must be >= 1");
+  if (o.backward_waves_per_wg < 1 || o.backward_waves_per_wg > 16)
+    return fail(EBAG_EINVAL, "backward_waves_per_wg must be in [1, 16]");
   return EBAG_OK;
 }
 
@@ -328,6 +331,8 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
   o->consumer_wgs = 512;
   o->stream_rows = 1;
   o->consume_timeout_us = 5000000;
+  o->backward_bags_per_run = 2;
+  o->backward_waves_per_wg = 8;
   return EBAG_OK;
 }
 
@@ -547,9 +552,15 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
   if (rc) return rc;
   int32_t max_dim = 0;
   for (const TabMeta& m : h->meta) max_dim = m.dim > max_dim ? m.dim : max_dim;
-  const int block = 64 * h->opts.waves_per_wg;
-  const size_t lds = (size_t)h->opts.waves_per_wg * max_dim * sizeof(float);
-  if (lds > 65536) return fail(EBAG_EUNSUPPORTED, "backward: waves_per_wg x widest row (%zu bytes) above 64 KiB", lds);
+  const int block = 64 * h->opts.backward_waves_per_wg;
+  // LDS holds the run's K gradient rows and K + 1 offsets: K is capped so
+  // that they fit in 64 KiB.
+  int32_t K = h->opts.backward_bags_per_run < h->C ? h->opts.backward_bags_per_run : h->C;
+  const int32_t k_fit = (int32_t)(65536 / ((size_t)max_dim * sizeof(float) + sizeof(int64_t)) - 1);
+  if (k_fit < 1) return fail(EBAG_EUNSUPPORTED, "backward: rows of %d floats do not fit in LDS", max_dim);
+  if (K > k_fit) K = k_fit;
+  if (K > block - 1) K = block - 1;
+  const size_t lds = (size_t)K * max_dim * sizeof(float) + (size_t)(K + 1) * sizeof(int64_t);
   BackwardArgs a;
   std::memset(&a, 0, sizeof a);
   a.grad = grad_buf;
@@ -566,7 +577,7 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
   a.so = so;
   a.T = h->T;
   a.C = h->C;
-  a.K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  a.K = K;
   a.J = (h->C + a.K - 1) / a.K;
   a.nruns = so.n_chunks * (int64_t)h->T * a.J;
   if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);

@@ -41,6 +41,7 @@ def test_default_opts(lib):
     import paper_2305_06942_amd as ebag
     o = ebag.default_opts()
     assert (o.waves_per_wg, o.rows_in_flight, o.debug_suppress_flag) == (4, 8, -1)
+    assert (o.backward_bags_per_run, o.backward_waves_per_wg) == (2, 8)
 
 
 def _create(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, max_batch=256, max_ranks=2, opts=None):
@@ -74,6 +75,7 @@ def test_create_rejects(lib, kw, msg):
     ("waves_per_wg", 0, "waves_per_wg"), ("waves_per_wg", 17, "waves_per_wg"),
     ("rows_in_flight", 5, "rows_in_flight"), ("bags_per_run", 0, "bags_per_run"),
     ("chunk_order", 2, "chunk_order"), ("consumer_wgs", 0, "consumer_wgs"),
+    ("backward_bags_per_run", 0, "backward_bags_per_run"), ("backward_waves_per_wg", 17, "backward_waves_per_wg"),
 ])
 def test_create_rejects_opts(lib, field, value, msg):
     import paper_2305_06942_amd as ebag

@@ -92,6 +92,34 @@ def test_backward_edge_cases(name):
     _check(inp, grad, values[:_n_values(inp)], False)
 
 
+_SHAPE_CASES = {
+    "tables_300": (synth.F32, [4, 8, 12] * 100, [5] * 300, 4, 2, 1, lambda r, n: r.integers(0, 4, n), True),
+    "chunk_128_wide": (synth.F32, [256, 1024], [50, 50], 256, 2, 128, lambda r, n: r.integers(0, 7, n), True),
+}
+
+
+@pytest.mark.parametrize("case", ["fp16_wide_ragged", "wide_rows_512", "many_tables", "tables_300", "chunk_128_wide"])
+@pytest.mark.parametrize("bags,waves", [(1, 1), (3, 2), (7, 16), (64, 4), (1000, 1)])
+def test_backward_launch_shapes(case, bags, waves):
+    """Bags per workgroup and workgroup sizes that put the per-thread walk over
+    the run's rows in every relation to the row width (step below, equal to,
+    above a row; several rows per step), bag counts past the LDS and thread
+    caps, and more tables than one pass of the table-size scan."""
+    import torch
+    spec = EDGE[case] if case in EDGE else _SHAPE_CASES[case]
+    inp = _custom_inputs(*spec, seed=len(case) + bags)
+    w = inp.w
+    dev = sdev.to_device(inp)
+    grad = _grad(w, bags * 17 + waves)
+    plan = make_plan(w, backward_bags_per_run=bags, backward_waves_per_wg=waves)
+    n = _n_values(inp)
+    values = torch.full((n + 64,), float("nan"), device="cuda")
+    plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
+    torch.cuda.synchronize()
+    _check(inp, grad, values[:n], False)
+    assert torch.isnan(values[n:]).all(), "stores past the last lookup row"
+
+
 def _fused(plan, w, dev, grad_dp, grad_recv, flags, values, epoch):
     import torch
     main = torch.cuda.current_stream()
