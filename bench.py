@@ -30,7 +30,8 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public specification
 KERNEL_SOURCES = {
     "fused_pool_kernel": ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
                           "paper_2305_06942_amd/csrc/repack_consume.hip"],
-    "backward_kernel": ["paper_2305_06942_amd/csrc/backward.hip", "paper_2305_06942_amd/csrc/common.h"],
+    "backward_kernel": ["paper_2305_06942_amd/csrc/backward.hip", "paper_2305_06942_amd/csrc/backward.h",
+                        "paper_2305_06942_amd/csrc/common.h"],
 }
 TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json"}
 # Plan options per workload.  Only the row-cache policy differs: workloads

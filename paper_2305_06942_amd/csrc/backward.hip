@@ -16,7 +16,7 @@
 // are contiguous (consecutive bags' lookups follow each other), so the whole
 // workgroup writes them as one block with 16-byte non-temporal stores,
 // balanced however the bag lengths vary.
-#include "common.h"
+#include "backward.h"
 
 namespace ebag {
 namespace {

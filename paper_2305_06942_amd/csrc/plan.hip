@@ -11,6 +11,7 @@
 
 #include "ebag_a2a.h"
 #include "common.h"
+#include "backward.h"
 
 using namespace ebag;
 
