@@ -171,7 +171,10 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
  * waits for: streams may share a hardware queue, and a consumer queued ahead
  * of its producer on the same queue can only time out.  Polling is bounded
  * by the plan's consume_timeout_us; on timeout the kernel stops and records
- * the first missing slice for ebag_a2a_status().
+ * the first missing slice for ebag_a2a_status().  expected_epoch is fixed
+ * when the call is made, so a graph replay could not wait for its own
+ * producer: on a stream under capture the call returns EBAG_EUNSUPPORTED
+ * and enqueues nothing.
  */
 int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags, float* recv_buf, int64_t B,
                      int32_t R, uint32_t expected_epoch, hipStream_t stream);
@@ -197,6 +200,10 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
  *     gets w_k * grad (sum; w_k = 1 without weights) or grad / L (mean), each
  *     value rounded once to fp32 -- the values of the sparse gradient of an
  *     EmbeddingBag, whose indices are the forward's indices.
+ * Launch shape: backward_bags_per_run bags per workgroup of
+ * backward_waves_per_wg wavefronts.  With grad_flags, on a stream under
+ * graph capture the call returns EBAG_EUNSUPPORTED (expected_epoch would be
+ * fixed for every replay); without flags it can be captured and replayed.
  */
 int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_flags, uint32_t expected_epoch,
                       const int64_t* offsets, const float* weights, int64_t B, int32_t R, float* values,

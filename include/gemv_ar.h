@@ -68,9 +68,11 @@ typedef struct gemv_ar_opts {
                                   failure-path tests; -1 (default) off */
   int32_t reduce_mode;         /* 0 (default): the last of the R ranks' workgroups p to store its partials
                                   for an owner reduces that owner's tiles (arrival counter, no waiting,
-                                  normal launch, P defaults to one tile per workgroup); 1: the owner's
-                                  workgroup waits for the peer flags and reduces (the paper's scheme;
-                                  cooperative launch, every workgroup resident) */
+                                  normal launch, P defaults to one tile per workgroup; can be captured
+                                  into a graph and replayed); 1: the owner's workgroup waits for the
+                                  peer flags and reduces (the paper's scheme; cooperative launch, every
+                                  workgroup resident; the flags carry a per-call epoch, so a forward on
+                                  a stream under graph capture returns EBAG_EUNSUPPORTED) */
   int64_t timeout_us;          /* reduce_mode 1: an owner gives up waiting after this long (default 5 s) */
 } gemv_ar_opts_t;
 

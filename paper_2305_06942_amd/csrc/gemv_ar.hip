@@ -530,6 +530,13 @@ int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, flo
   GemvArgs a;
   int rc = fill_args(h, A, x, y, out_flags, &a);
   if (rc) return rc;
+  if (h->opts.reduce_mode == 1) {
+    // The peer flags carry this call's epoch, fixed at capture: a graph
+    // replay would see the previous replay's flags and not wait.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+      return fail(EBAG_EUNSUPPORTED, "reduce_mode 1 cannot be captured into a graph (use reduce_mode 0)");
+  }
   // A fresh epoch per forward: peer flags of earlier forwards never match.
   // Epoch 0 is the value the flags start from, so it is skipped.
   if (++h->epoch == 0) ++h->epoch;

@@ -314,6 +314,14 @@ int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, bool weighted, 
 
 }  // namespace
 
+// Work that waits for a host-chosen epoch cannot be replayed from a graph:
+// the epoch is fixed at capture, so a replay would not wait for the flags of
+// its own producer.
+static bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
 extern "C" {
 
 int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
@@ -508,6 +516,8 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
     return fail(EBAG_EINVAL, "bad B=%lld / R=%d for this plan", (long long)B, R);
   if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
     return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
+  if (capturing(stream))
+    return fail(EBAG_EUNSUPPORTED, "consume waits for a fixed epoch; it cannot be captured into a graph");
   ConsumeArgs c;
   std::memset(&c, 0, sizeof c);
   c.send = send_buf;
@@ -548,6 +558,8 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
   if (!grad_buf || !offsets || !values) return fail(EBAG_EINVAL, "null grad_buf, offsets or values");
   if (!aligned16(grad_buf) || !aligned16(values)) return fail(EBAG_EINVAL, "grad_buf or values not 16-byte aligned");
   if (weights && h->opts.pooling_mode == 1) return fail(EBAG_EINVAL, "mean pooling takes no weights");
+  if (grad_flags && capturing(stream))
+    return fail(EBAG_EUNSUPPORTED, "backward with flags waits for a fixed epoch; it cannot be captured into a graph");
   SliceOrder so;
   int rc = check_split(h, B, R, &so);
   if (rc) return rc;
