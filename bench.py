@@ -457,7 +457,36 @@ def backward_bytes(w, lengths, weighted):
     return rows + 4 * w.B * w.sum_dim + 8 * (w.T * w.B + 1) + (4 * nnz if weighted else 0)
 
 
-def run_backward(name, steps, warmup, profile=False):
+def backward_cpu_baseline(w, inp, grad, mean=False, max_bytes=2 << 30, min_seconds=10.0):
+    """The C oracle's embedding backward (one thread) timed on this host over
+    the first tables of the workload whose per-lookup rows fit in max_bytes
+    (all B samples of each), repeated until about min_seconds."""
+    import numpy as np
+    import oracle
+    L = inp.lengths.reshape(w.T, w.B).sum(axis=1)
+    T, acc = 0, 0
+    while T < w.T and acc + int(L[T]) * w.dims[T] * 4 <= max_bytes:
+        acc += int(L[T]) * w.dims[T] * 4
+        T += 1
+    T = max(T, 1)
+    sub = w.with_(T=T, rows=w.rows[:T], dims=w.dims[:T])
+    off = inp.offsets[:T * w.B + 1]
+    nnz = int(off[-1])
+    wts = None if inp.weights is None else inp.weights[:nnz]
+    g = np.ascontiguousarray(grad[:, :sub.sum_dim])
+    nbytes = backward_bytes(sub, inp.lengths[:T * w.B], wts is not None)
+    times = []
+    while len(times) < 3 or sum(times) < min_seconds:
+        t0 = time.time()
+        oracle.backward(sub.dims, off, wts, g, w.B, w.R, mean=mean)
+        times.append(time.time() - t0)
+    med = sorted(times)[len(times) // 2]
+    return {"value": round(nbytes / med / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"C oracle (one thread) over tables 0..{T - 1} of {w.T}, all {w.B} samples "
+                      f"({nbytes / 1e9:.2f} GB algorithmic), median of {len(times)} passes ({sum(times):.1f} s in all)"}
+
+
+def run_backward(name, steps, warmup, profile=False, with_cpu=True):
     """Embedding backward: the kernel alone (gradient complete), the
     bulk-synchronous sequence (delivery of the gradient, then the backward)
     and the fused one (backward expanding slices as the delivery lands).
@@ -531,6 +560,8 @@ def run_backward(name, steps, warmup, profile=False):
                         "unit": "GB/s", "frac": round(nbytes / (k_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                         "traffic": tr["hbm_bytes_per_launch"] if tr else None},
            "data": "synthetic: the workload's bags, a seeded torch.randn pooled gradient"}
+    if with_cpu:
+        row["cpu_baseline"] = backward_cpu_baseline(w, inp, grad_dp.cpu().numpy())
     print(json.dumps(row), flush=True)
     plan.close()
     return row
@@ -745,7 +776,7 @@ def main():
         return 0
     if a.backward:
         for n in (["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
-            run_backward(n, a.steps, a.warmup, profile=a.profile)
+            run_backward(n, a.steps, a.warmup, profile=a.profile, with_cpu=not a.no_cpu_baseline)
         return 0
     if a.gemv_ar:
         shapes = [sh for sh in GEMV_SHAPES if a.gemv_m in (0, sh[0])]
