@@ -122,7 +122,8 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* opts);
  *   rows_per_table[T], dim_per_table[T]: host arrays; rows >= 0 (< 2^31), D > 0,
  *     D * elt % 16 == 0.
  *   table_dtype: storage type shared by all tables; pooled output is fp32.
- *   chunk_samples (C): samples per slice, > 0.
+ *   chunk_samples (C): samples per slice, > 0; one slice (C * sum(D) fp32)
+ *     must be below 2 GiB.
  *   max_batch: largest B any forward will use (sizes the slice counters and
  *     the unfused scratch of max_batch * sum(D) floats).
  *   max_ranks: largest R any forward will use.

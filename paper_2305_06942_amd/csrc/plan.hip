@@ -383,6 +383,10 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   }
   if (sum_dim > INT32_MAX / 4) return fail(EBAG_EINVAL, "sum of dims too large");
   if ((int64_t)max_batch * sum_dim > (int64_t)1 << 40) return fail(EBAG_EINVAL, "max_batch * sum(D) too large");
+  // A slice is one message: the per-table consumer and delivery address it
+  // with 32-bit byte offsets.
+  if ((int64_t)chunk_samples * sum_dim * 4 > INT32_MAX)
+    return fail(EBAG_EINVAL, "a slice (chunk_samples x sum(D) fp32) must be below 2 GiB");
 
   ebag_a2a_plan* h = new (std::nothrow) ebag_a2a_plan();
   if (!h) return fail(EBAG_ENOMEM, "host allocation failed");

@@ -62,6 +62,7 @@ def _create(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, max_batch=256
     (dict(C=0), "chunk_samples"),
     (dict(max_batch=0), "max_batch"),
     (dict(rows=(10, -1)), "rows"),
+    (dict(dims=(1 << 20, 1 << 20), C=1024, max_batch=2048), "below 2 GiB"),
 ])
 def test_create_rejects(lib, kw, msg):
     import paper_2305_06942_amd as ebag
