@@ -149,6 +149,32 @@ def probe_ceiling(w, lengths, weighted, nt):
     return alg / (us * 1e-6) / 1e9, us
 
 
+def run_stream_probe(reps=20):
+    """Streaming ceilings: reads (synth_stream_read, 16-byte non-temporal
+    loads, 8 in flight per lane; best of several grid sizes) and writes
+    (torch fill_) of 256 MiB, 1 GiB and 4 GiB."""
+    import torch
+    from synth import device as sdev
+    s = torch.cuda.current_stream()
+    rows = []
+    for nbytes in (256 << 20, 1 << 30, 4 << 30):
+        buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        best = None
+        for grid in (1024, 2048, 4096, 8192, 16384):
+            out = torch.empty(grid * 256, dtype=torch.int32, device="cuda")
+            sdev.stream_read(buf, grid, out)
+            ms = time_launches(lambda: sdev.stream_read(buf, grid, out), reps, s)
+            if best is None or ms < best[1]:
+                best = (grid, ms)
+        fill_ms = time_launches(lambda: buf.fill_(2.0), reps, s)
+        row = {"bytes": nbytes, "read_gbs": round(nbytes / best[1] / 1e6, 1), "read_grid": best[0],
+               "write_gbs": round(nbytes / fill_ms / 1e6, 1)}
+        rows.append(row)
+        print(json.dumps(row), flush=True)
+        del buf
+    return rows
+
+
 def run_row_probe():
     rows = []
     for rb in (64, 128, 256, 512, 1024):
@@ -744,6 +770,7 @@ def main():
     ap.add_argument("--gemv-m", type=int, default=0, help="with --gemv-ar: only the shape with this M")
     ap.add_argument("--backward", action="store_true", help="embedding backward fused with the gradient's arrival")
     ap.add_argument("--backward-sweep", action="store_true", help="backward kernel time per launch shape")
+    ap.add_argument("--stream-probe", action="store_true", help="streaming read and write ceilings")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize))
@@ -766,6 +793,9 @@ def main():
         return 0
     if a.timeline:
         run_timeline(a.workload, a.warmup)
+        return 0
+    if a.stream_probe:
+        run_stream_probe()
         return 0
     if a.row_probe:
         run_row_probe()

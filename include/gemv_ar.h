@@ -62,7 +62,7 @@ typedef struct gemv_ar_opts {
   int32_t wgs_per_rank;        /* physical workgroups per rank P, at most the number of tiles; 0 (default):
                                   one per tile (reduce_mode 0) or as many as can be resident at once for
                                   the whole grid (reduce_mode 1) */
-  int32_t waves_per_wg;        /* wavefronts per workgroup, 1..16 (default 4) */
+  int32_t waves_per_wg;        /* wavefronts per workgroup, 1..16 (default 2) */
   int32_t comm_aware;          /* 1 (default): tiles owned by other ranks first; 0: tile order */
   int32_t debug_suppress_flag; /* >= 0: never set this peer flag ((owner * R + rank) * P + p), for
                                   failure-path tests; -1 (default) off */

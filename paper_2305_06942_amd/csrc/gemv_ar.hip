@@ -431,7 +431,7 @@ int gemv_ar_default_opts(gemv_ar_opts_t* o) {
   std::memset(o, 0, sizeof *o);
   o->tile_rows = 128;
   o->wgs_per_rank = 0;
-  o->waves_per_wg = 4;
+  o->waves_per_wg = 2;
   o->comm_aware = 1;
   o->debug_suppress_flag = -1;
   o->reduce_mode = 0;

@@ -35,6 +35,8 @@ def load():
         lib.synth_gather_probe.argtypes = [P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                            ctypes.c_int32, P, P]
         lib.synth_gather_probe.restype = ctypes.c_int
+        lib.synth_stream_read.argtypes = [P, ctypes.c_int64, ctypes.c_int32, P, P]
+        lib.synth_stream_read.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -112,3 +114,17 @@ def gather_probe(buf, row_bytes: int, steps: int, grid: int, out, nt: bool = Tru
     if rc != 0:
         raise RuntimeError(f"synth_gather_probe failed: {rc}")
     return grid * 4 * steps * 1024
+
+
+def stream_read(buf, grid: int, out, stream=None) -> int:
+    """Streaming read of every byte of ``buf`` (see synth/fill.hip); returns
+    the bytes it reads."""
+    import torch
+    s = torch.cuda.current_stream().cuda_stream if stream is None else stream
+    nbytes = buf.numel() * buf.element_size()
+    if out.numel() * out.element_size() < grid * 256 * 4:
+        raise ValueError("probe output too small")
+    rc = load().synth_stream_read(buf.data_ptr(), nbytes, grid, out.data_ptr(), s)
+    if rc != 0:
+        raise RuntimeError(f"synth_stream_read failed: {rc}")
+    return nbytes

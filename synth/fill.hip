@@ -120,6 +120,25 @@ __global__ __launch_bounds__(256) void gather_probe_kernel(const char* __restric
   out[(uint64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
 }
 
+// Streaming reads: the grid walks base[0 : n16 * 16) in 16-byte vectors,
+// thread i reading vectors i, i + stride, ... with 8 non-temporal loads in
+// flight, folded into one word per thread so the loads cannot be dropped.
+__global__ __launch_bounds__(256) void stream_read_kernel(const u4v* __restrict__ p, uint64_t n16,
+                                                          uint32_t* __restrict__ out) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  u4v acc = {0u, 0u, 0u, 0u};
+  for (; i + 7 * stride < n16; i += 8 * stride) {
+    u4v r[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) r[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc ^= r[u];
+  }
+  for (; i < n16; i += stride) acc ^= __builtin_nontemporal_load(p + i);
+  out[(uint64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc.x ^ acc.y ^ acc.z ^ acc.w;
+}
+
 }  // namespace
 
 extern "C" {
@@ -167,6 +186,15 @@ int synth_gather_probe(const void* base, int64_t bytes, int32_t row_bytes, int32
   else
     hipLaunchKernelGGL(gather_probe_kernel<false>, dim3(grid), dim3(256), 0, stream, (const char*)base, nrows,
                        lshift, steps, (uint32_t*)out);
+  return (int)hipGetLastError();
+}
+
+// Streaming read probe over base[0:bytes) (bytes a multiple of 16, base
+// 16-byte aligned): grid workgroups of 256 threads.  out: grid * 256 uint32.
+int synth_stream_read(const void* base, int64_t bytes, int32_t grid, void* out, hipStream_t stream) {
+  if (!base || !out || bytes <= 0 || (bytes & 15) || ((uintptr_t)base & 15) || grid <= 0) return -1;
+  hipLaunchKernelGGL(stream_read_kernel, dim3(grid), dim3(256), 0, stream, (const u4v*)base, (uint64_t)bytes / 16,
+                     (uint32_t*)out);
   return (int)hipGetLastError();
 }
 
