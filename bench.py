@@ -647,7 +647,7 @@ def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
         x = [torch.randn((k,), generator=g, device="cuda").to(tdt) for k in Ks]
         y = [torch.empty((M,), device="cuda") for _ in range(R)]
         plan = ebag.GemvAR(R, M, Ks, dtype)
-        P, block, n_tiles, resident = plan.launch_info()
+        P, block, n_tiles, resident, tile_rows = plan.launch_info()
         flags = torch.zeros(R * P, dtype=torch.int32, device="cuda")
         fused = lambda: plan.forward(A, x, y, flags)
         unfused = lambda: plan.unfused_forward(A, x, y, flags)
@@ -659,7 +659,7 @@ def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
         assert plan.status() == (0, -1)
         nbytes = gemv_ar_bytes(R, M, K, elt)
         row = {"operator": "gemv_allreduce", "ranks": R, "M": M, "K": K, "dtype": {0: "f32", 1: "f16", 2: "bf16"}[dtype],
-               "tile_rows": plan.opts.tile_rows, "wgs_per_rank": P, "threads_per_wg": block,
+               "tile_rows": tile_rows, "wgs_per_rank": P, "threads_per_wg": block,
                "fused_us": round(f_ms * 1e3, 2), "unfused_us": round(u_ms * 1e3, 2),
                "fused_speedup_vs_unfused": round(u_ms / f_ms, 4), "algorithmic_bytes": nbytes,
                "roofline": {"bound": "hbm", "achieved": round(nbytes / (f_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,

@@ -58,7 +58,8 @@ extern "C" {
 typedef struct gemv_ar_plan* gemv_ar_t;
 
 typedef struct gemv_ar_opts {
-  int32_t tile_rows;           /* rows per output tile, 1..4096 (default 128) */
+  int32_t tile_rows;           /* rows per output tile, 1..4096; 0 (default): 128, halved down to 32 while
+                                  the R ranks have fewer than 1024 tiles in all */
   int32_t wgs_per_rank;        /* physical workgroups per rank P, at most the number of tiles; 0 (default):
                                   one per tile (reduce_mode 0) or as many as can be resident at once for
                                   the whole grid (reduce_mode 1) */
@@ -114,8 +115,8 @@ int gemv_ar_reset(gemv_ar_t h);
 
 /* Launch shape: out[0] P (workgroups per rank), out[1] threads per
  * workgroup, out[2] number of tiles, out[3] workgroups the device can hold
- * resident at once for this kernel. */
-int gemv_ar_launch_info(gemv_ar_t h, int32_t out[4]);
+ * resident at once for this kernel, out[4] rows per tile. */
+int gemv_ar_launch_info(gemv_ar_t h, int32_t out[5]);
 
 /* Release the plan's device memory.  NULL is ignored. */
 void gemv_ar_destroy(gemv_ar_t h);

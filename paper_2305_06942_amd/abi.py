@@ -300,8 +300,8 @@ class GemvAR:
         _check(self._lib.gemv_ar_reset(self._h))
 
     def launch_info(self):
-        """(workgroups per rank P, threads per workgroup, tiles, resident workgroups)."""
-        s = (ctypes.c_int32 * 4)()
+        """(workgroups per rank P, threads per workgroup, tiles, resident workgroups, rows per tile)."""
+        s = (ctypes.c_int32 * 5)()
         _check(self._lib.gemv_ar_launch_info(self._h, s))
         return tuple(s)
 

@@ -429,7 +429,7 @@ extern "C" {
 int gemv_ar_default_opts(gemv_ar_opts_t* o) {
   if (!o) return fail(EBAG_EINVAL, "null opts");
   std::memset(o, 0, sizeof *o);
-  o->tile_rows = 128;
+  o->tile_rows = 0;
   o->wgs_per_rank = 0;
   o->waves_per_wg = 2;
   o->comm_aware = 1;
@@ -449,7 +449,13 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   if (dtype != EBAG_F32 && dtype != EBAG_F16 && dtype != EBAG_BF16) return fail(EBAG_EINVAL, "bad dtype %d", (int)dtype);
   gemv_ar_opts_t o;
   if (opts) o = *opts; else gemv_ar_default_opts(&o);
-  if (o.tile_rows < 1 || o.tile_rows > 4096) return fail(EBAG_EINVAL, "tile_rows must be in [1, 4096]");
+  if (o.tile_rows < 0 || o.tile_rows > 4096) return fail(EBAG_EINVAL, "tile_rows must be 0 (auto) or in [1, 4096]");
+  if (o.tile_rows == 0) {
+    // 128-row tiles, halved (down to 32) until the R ranks' tiles give at
+    // least 1024 workgroups: enough to cover launch and tail on 256 CUs.
+    o.tile_rows = 128;
+    while (o.tile_rows > 32 && (int64_t)R * ((M + o.tile_rows - 1) / o.tile_rows) < 1024) o.tile_rows /= 2;
+  }
   if (o.waves_per_wg < 1 || o.waves_per_wg > 16) return fail(EBAG_EINVAL, "waves_per_wg must be in [1, 16]");
   if (o.wgs_per_rank < 0) return fail(EBAG_EINVAL, "wgs_per_rank must be >= 0");
   if (o.comm_aware != 0 && o.comm_aware != 1) return fail(EBAG_EINVAL, "comm_aware must be 0 or 1");
@@ -598,12 +604,13 @@ int gemv_ar_reset(gemv_ar_t h) {
   return EBAG_OK;
 }
 
-int gemv_ar_launch_info(gemv_ar_t h, int32_t out[4]) {
+int gemv_ar_launch_info(gemv_ar_t h, int32_t out[5]) {
   if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
   out[0] = h->P;
   out[1] = h->block;
   out[2] = (int32_t)(h->n_tiles > INT_MAX ? INT_MAX : h->n_tiles);
   out[3] = h->resident;
+  out[4] = h->opts.tile_rows;
   return EBAG_OK;
 }
 

@@ -126,5 +126,5 @@ def test_gemv_null_plan_rejected(lib):
     assert lib.gemv_ar_unfused_forward(None, None, None, None, None, None) == ebag.abi.EBAG_EINVAL
     assert lib.gemv_ar_reset(None) == ebag.abi.EBAG_EINVAL
     o = ebag.gemv_default_opts()
-    assert (o.tile_rows, o.waves_per_wg, o.comm_aware, o.debug_suppress_flag, o.reduce_mode) == (128, 2, 1, -1, 0)
+    assert (o.tile_rows, o.waves_per_wg, o.comm_aware, o.debug_suppress_flag, o.reduce_mode) == (0, 2, 1, -1, 0)
     lib.gemv_ar_destroy(None)

@@ -65,7 +65,8 @@ def _run(R, M, Ks, dtype, seed, integer=False, epochs=2, **opts):
     dA = [_to_dev(a, dtype) for a in A]
     dx = [_to_dev(v, dtype) for v in x]
     plan = ebag.GemvAR(R, M, Ks, dtype, **opts)
-    P, block, n_tiles, resident = plan.launch_info()
+    P, block, n_tiles, resident, tile_rows = plan.launch_info()
+    assert n_tiles == -(-M // tile_rows)
     assert 1 <= P <= n_tiles and (opts.get("reduce_mode", 0) == 0 or R * P <= resident)
     rel = _depth(R, Ks, dtype) * 2.0 ** -24
     outs = []
