@@ -7,6 +7,9 @@ import oracle
 import synth
 from synth import device as sdev
 from tests.gpu_util import check_full, flags_np, make_plan, new_buffers, run, say
+from tests.test_gpu_parity import SMALL
+
+SMALL_MIXED = SMALL["mixed_small"]
 
 pytestmark = pytest.mark.gpu
 
@@ -177,3 +180,66 @@ def test_bad_index_reported_and_skipped():
     st = plan.status_ex()
     assert st[3] == bad_bag
     assert np.all(flags_np(flags) == 1)
+
+
+@pytest.mark.parametrize("opts", [dict(), dict(slice_granule=1), dict(persistent_wgs_per_cu=-1, chunk_order=1,
+                                                                      self_rank=3)],
+                         ids=["default", "per_table", "persistent_comm_aware"])
+def test_stress_100_epochs_across_flag_wraparound(opts):
+    """100 forwards, each drained concurrently by the consumer, with the epoch
+    flags starting 50 below 2^32 so that they wrap to 0 midway: every epoch
+    must be fully drained (recv == send bit for bit, sentinel-filled before),
+    with every flag at the epoch and no timeout or double publication."""
+    import torch
+    w = SMALL_MIXED
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, **opts)
+    send, recv, _ = new_buffers(w)
+    base = (1 << 32) - 50
+    flags = torch.full((plan.n_flags(w.B),), base - (1 << 32), dtype=torch.int32, device="cuda")
+    say("stress", opts)
+    for k in range(1, 101):
+        epoch = (base + k) & 0xFFFFFFFF
+        recv.fill_(float("nan"))
+        _concurrent(plan, w, dev, send, recv, flags, epoch)
+        assert torch.equal(send.view(torch.int32), recv.view(torch.int32)), f"epoch {k}"
+        assert np.all(flags_np(flags) == epoch), f"epoch {k}"
+    assert plan.status_ex() == (0, -1, 0, -1)
+    check_full(inp, send.cpu().numpy())
+
+
+def test_stress_100_backward_epochs_across_flag_wraparound():
+    """100 backwards, each fed by the delivery stand-in on its own queue and
+    waiting per slice, flags wrapping through 2^32: every epoch equals the
+    bulk-synchronous result bit for bit."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    w = SMALL_MIXED
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    n = int(sum((inp.offsets[(t + 1) * w.B] - inp.offsets[t * w.B]) * w.dims[t] for t in range(w.T)))
+    grad = torch.randn((w.B, w.sum_dim), generator=torch.Generator(device="cuda").manual_seed(3), device="cuda")
+    want = torch.empty((n,), device="cuda")
+    plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, want)
+    torch.cuda.synchronize()
+    base = (1 << 32) - 50
+    flags = torch.full((w.n_chunks,), base - (1 << 32), dtype=torch.int32, device="cuda")
+    recv = torch.empty_like(grad)
+    values = torch.empty_like(want)
+    main = torch.cuda.current_stream()
+    send_q, bwd_q = ebag.queue_stream(), ebag.queue_stream()
+    for k in range(1, 101):
+        epoch = (base + k) & 0xFFFFFFFF
+        recv.fill_(float("nan"))
+        values.fill_(float("nan"))
+        send_q.wait_stream(main)
+        bwd_q.wait_stream(main)
+        with torch.cuda.stream(send_q):
+            plan.deliver(grad, recv, flags, w.B, w.R)
+        with torch.cuda.stream(bwd_q):
+            plan.backward(recv, dev.offsets, dev.weights, w.B, w.R, values, grad_flags=flags, expected_epoch=epoch)
+        torch.cuda.synchronize()
+        assert torch.equal(values.view(torch.int32), want.view(torch.int32)), f"epoch {k}"
+    assert plan.status_ex() == (0, -1, 0, -1)
