@@ -385,7 +385,49 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
     if with_cpu:
         log(f"[{name}] timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes, mean=mean)
+    out["env"] = env_info(inp)
     return out
+
+
+def git_head():
+    """The checked-out commit, read from .git without running git (None when
+    the tree has no .git)."""
+    try:
+        with open(os.path.join(ROOT, ".git", "HEAD")) as f:
+            head = f.read().strip()
+        if head.startswith("ref: "):
+            ref = head[5:]
+            path = os.path.join(ROOT, ".git", ref)
+            if os.path.exists(path):
+                with open(path) as f:
+                    return f.read().strip()[:12]
+            with open(os.path.join(ROOT, ".git", "packed-refs")) as f:
+                for line in f:
+                    if line.strip().endswith(" " + ref):
+                        return line.split()[0][:12]
+            return None
+        return head[:12]
+    except OSError:
+        return None
+
+
+def env_info(inp=None):
+    """Where and on what the numbers were taken: device, architecture, HIP
+    and torch versions, the hash of the pooling kernels' sources, the git
+    commit when the tree has one, and a digest of the workload's inputs."""
+    import torch
+    props = torch.cuda.get_device_properties(0)
+    env = {"device": torch.cuda.get_device_name(0), "arch": getattr(props, "gcnArchName", None),
+           "cus": props.multi_processor_count, "hip": torch.version.hip, "torch": torch.__version__,
+           "kernel_sources": kernel_hash()}
+    env["git"] = git_head()
+    if inp is not None:
+        h = hashlib.sha256()
+        for a in (inp.offsets, inp.indices, inp.weights):
+            if a is not None:
+                h.update(a.tobytes())
+        env["inputs_sha256"] = h.hexdigest()[:16]
+    return env
 
 
 def _setup(name):
@@ -588,6 +630,7 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
            "data": "synthetic: the workload's bags, a seeded torch.randn pooled gradient"}
     if with_cpu:
         row["cpu_baseline"] = backward_cpu_baseline(w, inp, grad_dp.cpu().numpy())
+    row["env"] = env_info(inp)
     print(json.dumps(row), flush=True)
     plan.close()
     return row
@@ -679,6 +722,7 @@ def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
                                    "cores": len(os.sched_getaffinity(0)), "kind": "oracle",
                                    "sample": f"C oracle (fp64) over the whole {M} x {K} problem, median of "
                                              f"{len(times)} passes, {med:.3f} s per pass"}
+        row["env"] = env_info()
         out.append(row)
         print(json.dumps(row), flush=True)
         plan.close()
