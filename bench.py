@@ -34,15 +34,17 @@ KERNEL_SOURCES = {
                         "paper_2305_06942_amd/csrc/common.h"],
 }
 TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json"}
-# Plan options per workload.  Only the row-cache policy differs: workloads
-# whose indices follow a skewed (Zipf) law re-read hot rows, so their table
-# rows are read through the caches; uniform workloads stream rows (default).
 # Launch options per workload (every other option at its default):
 #  * Zipf-distributed indices reuse hot rows, so the Zipf workloads read rows
-#    through the caches (stream_rows = 0) rather than streaming them;
+#    through the caches (stream_rows = 0) rather than streaming them, and go
+#    table by table (table_major = 1, each XCD working through its own
+#    tables) with the paper's per-table slices (slice_granule = 1), so a
+#    table's hot rows stay cached while it is pooled;
 #  * mixed has many short runs (64-byte rows, variable lengths): a persistent
 #    grid claiming runs from the ticket beats one workgroup per run there.
-PLAN_OPTS = {"skewed": {"stream_rows": 0}, "large": {"stream_rows": 0}, "mixed": {"persistent_wgs_per_cu": -1}}
+PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1},
+             "large": {"stream_rows": 0, "table_major": 1, "slice_granule": 1},
+             "mixed": {"persistent_wgs_per_cu": -1}}
 PAPER_CONTEXT = ("the paper's fused embedding + All-to-All reduced execution time by 20% intra-node "
                  "(4x MI210 over Infinity Fabric, 80 GB/s) and 31% inter-node (2x MI210 over InfiniBand, "
                  "20 GB/s); context only, those numbers include real inter-GPU transport")
@@ -286,7 +288,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
         opts["pooling_mode"] = 1
     if per_table:
         opts["slice_granule"] = 1
-    n_flags = w.n_chunks * (w.T if per_table else 1)
+    per_table_slices = opts.get("slice_granule", 0) == 1
+    n_flags = w.n_chunks * (w.T if per_table_slices else 1)
     alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None, n_flags)
     plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **opts)
     send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
@@ -329,7 +332,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
                    "storage": {0: "f32", 1: "f16", 2: "bf16"}[w.dtype], "global_batch": w.B,
                    "bag_lengths": w.lengths, "indices": w.indices, "weighted": w.weighted,
                    "pooling": "mean" if mean else "sum",
-                   "slices": "per table" if per_table else "all tables",
+                   "slices": "per table" if per_table_slices else "all tables",
+                   "run_order": "table-major" if opts.get("table_major") else "slice-major",
                    "destinations": w.R, "slice_samples": w.C, "parallelism": "1 GPU, R logical destinations"},
         "fused_us": round(fused_ms * 1e3, 2),
         "unfused_us": round(unfused_ms * 1e3, 2),
@@ -438,7 +442,7 @@ def _setup(name):
     inp = synth.make_inputs(w)
     dev = sdev.to_device(inp)
     send = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
-    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(w.n_chunks * w.T, dtype=torch.int32, device="cuda")  # room for per-table slices
     return w, inp, dev, send, flags
 
 
@@ -485,7 +489,8 @@ def run_timeline(name, warmup):
     import paper_2305_06942_amd as ebag
     w, inp, dev, send, flags = _setup(name)
     recv = torch.empty_like(send)
-    base = dict(PLAN_OPTS.get(name, {}))
+    # whole slices in slice-major order: the study is the order of slices
+    base = {k: v for k, v in PLAN_OPTS.get(name, {}).items() if k not in ("slice_granule", "table_major")}
     prod, cons = ebag.queue_stream(), ebag.queue_stream()
     stream = torch.cuda.current_stream()
     epoch = [0]
@@ -572,7 +577,7 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
     g = torch.Generator(device="cuda").manual_seed(2305)
     grad_dp = torch.randn((w.B, w.sum_dim), generator=g, device="cuda")
     grad_recv = torch.empty_like(grad_dp)
-    flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+    flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
     s = torch.cuda.current_stream()
     nbytes = backward_bytes(w, inp.lengths, inp.weights is not None)
     bwd = lambda: plan.backward(grad_recv, dev.offsets, dev.weights, w.B, w.R, values)

@@ -112,6 +112,13 @@ typedef struct ebag_a2a_opts {
   int32_t backward_bags_per_run;  /* ebag_a2a_backward: bags per workgroup (default 2; capped so that the
                                      bags' gradient rows fit in 64 KiB of LDS) */
   int32_t backward_waves_per_wg;  /* ebag_a2a_backward: wavefronts per workgroup, 1..16 (default 8) */
+  int32_t table_major;         /* 0 (default): runs slice by slice, tables fastest inside a slice; 1: table
+                                  by table, slices in order inside each table, and (when T is a multiple
+                                  of the XCD count) each XCD working through its own tables one at a time,
+                                  so that a table's hot rows stay in that XCD's caches.  Meant for
+                                  slice_granule = 1, whose per-table slices then still complete
+                                  progressively; with whole slices every slice completes at the end.  The
+                                  consumer, backward and delivery follow the same order. */
 } ebag_a2a_opts_t;
 
 /* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */

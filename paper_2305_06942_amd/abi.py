@@ -37,6 +37,7 @@ class Opts(ctypes.Structure):
         ("slice_granule", ctypes.c_int32),
         ("backward_bags_per_run", ctypes.c_int32),
         ("backward_waves_per_wg", ctypes.c_int32),
+        ("table_major", ctypes.c_int32),
     ]
 
 
@@ -137,6 +138,13 @@ def _stream(stream) -> Optional[int]:
     return stream.cuda_stream
 
 
+def _need(buf, nbytes: int, what: str):
+    """A torch tensor passed as a buffer must hold at least nbytes (raw
+    integer addresses are the caller's responsibility)."""
+    if buf is not None and hasattr(buf, "numel") and buf.numel() * buf.element_size() < nbytes:
+        raise ValueError(f"{what} holds {buf.numel() * buf.element_size()} bytes, needs {nbytes}")
+
+
 def queue_stream():
     """A torch stream on a hardware queue of its own (ebag_a2a_queue_stream_create)."""
     import torch
@@ -183,25 +191,36 @@ class Plan:
             self._tab_cache = (ptrs, (ctypes.c_void_p * self.T)(*ptrs))
         return self._tab_cache[1]
 
+    def _fwd_sizes(self, B, send, flags):
+        _need(send, 4 * int(B) * sum(self.dims), "send buffer")
+        _need(flags, 4 * self.n_flags(int(B)), "flags")
+
     def forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
+        self._fwd_sizes(B, send, flags)
         _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
                                           _addr(weights), int(B), int(R), _addr(send), _addr(flags), _stream(stream)))
 
     def unfused_forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
+        self._fwd_sizes(B, send, flags)
         _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
                                                   _addr(weights), int(B), int(R), _addr(send), _addr(flags),
                                                   _stream(stream)))
 
     def consume(self, send, flags, recv, B, R, expected_epoch, stream=None):
+        self._fwd_sizes(B, send, flags)
+        _need(recv, 4 * int(B) * sum(self.dims), "recv buffer")
         _check(self._lib.ebag_a2a_consume(self._h, _addr(send), _addr(flags), _addr(recv), int(B), int(R),
                                           int(expected_epoch) & 0xFFFFFFFF, _stream(stream)))
 
     def backward(self, grad, offsets, weights, B, R, values, grad_flags=None, expected_epoch=0, stream=None):
+        self._fwd_sizes(B, grad, grad_flags)
         _check(self._lib.ebag_a2a_backward(self._h, _addr(grad), _addr(grad_flags), int(expected_epoch) & 0xFFFFFFFF,
                                            _addr(offsets), _addr(weights), int(B), int(R), _addr(values),
                                            _stream(stream)))
 
     def deliver(self, src, dst, flags, B, R, stream=None):
+        self._fwd_sizes(B, src, flags)
+        _need(dst, 4 * int(B) * sum(self.dims), "destination buffer")
         _check(self._lib.ebag_a2a_deliver(self._h, _addr(src), _addr(dst), _addr(flags), int(B), int(R),
                                           _stream(stream)))
 
@@ -280,11 +299,18 @@ class GemvAR:
         arr = ctypes.c_void_p * self.R
         return arr(*[_addr(a) for a in A]), arr(*[_addr(v) for v in x]), arr(*[_addr(v) for v in y])
 
+    def _out_sizes(self, y, out_flags):
+        for v in y:
+            _need(v, 4 * self.M, "output vector")
+        _need(out_flags, 4 * self.R * self.launch_info()[0], "out_flags")
+
     def forward(self, A, x, y, out_flags=None, stream=None):
+        self._out_sizes(y, out_flags)
         a, xv, yv = self._arrays(A, x, y)
         _check(self._lib.gemv_ar_forward(self._h, a, xv, yv, _addr(out_flags), _stream(stream)))
 
     def unfused_forward(self, A, x, y, out_flags=None, stream=None):
+        self._out_sizes(y, out_flags)
         a, xv, yv = self._arrays(A, x, y)
         _check(self._lib.gemv_ar_unfused_forward(self._h, a, xv, yv, _addr(out_flags), _stream(stream)))
 

@@ -64,12 +64,9 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   extern __shared__ f4v s_lds[];
   __shared__ int s_bad;
   const int tid = threadIdx.x;
-  const int64_t per_slice = (int64_t)a.T * a.J;
-  const int64_t q = blockIdx.x;
-  const int64_t gs = q / per_slice;
-  const int64_t rem = q - gs * per_slice;
-  const int tpos = (int)(rem % a.T);
-  const int j = (int)(rem / a.T);
+  int64_t gs;
+  int32_t tpos, j;
+  run_at(a.so, a.T, a.J, blockIdx.x, &gs, &tpos, &j);
   const int t = sld(a.tperm, tpos);
   const int64_t g = slice_at(a.so, gs);
   if (a.flags) {
@@ -152,8 +149,15 @@ __global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
   const int64_t per_slice = a.per_table ? a.T : a.pieces;
   const int64_t n_items = a.so.n_chunks * per_slice;
   for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
-    const int64_t gs = x / per_slice;
-    const int64_t p = x - gs * per_slice;
+    int64_t gs, p;
+    if (a.per_table) {  // (slice, table) items in production order
+      int32_t tp, unused;
+      run_at(a.so, a.T, 1, x, &gs, &tp, &unused);
+      p = tp;
+    } else {
+      gs = x / per_slice;
+      p = x - gs * per_slice;
+    }
     const int64_t g = slice_at(a.so, gs);
     if (a.per_table) {
       const int t = __builtin_amdgcn_readfirstlane(a.tperm[p]);

@@ -19,13 +19,16 @@ struct TabMeta {
 // Order in which slices are produced and drained.  order 0: natural; order
 // 1: slices of destination `self` last, so slices bound for other
 // destinations are finished (and can be shipped) first (Sec. III-A,
-// communication-aware scheduling).
+// communication-aware scheduling).  table_groups 0: runs go slice by slice,
+// table positions fastest; G >= 1: table by table, slices (in the order
+// above) inside a table, with run q taken by table group q mod G -- with G
+// the number of XCDs, every XCD works through its own tables one at a time.
 struct SliceOrder {
   int64_t n_chunks;    // B / C
   int64_t per_rank;    // (B / R) / C
   int64_t self;        // destination kept local
   int32_t order;
-  int32_t pad;
+  int32_t table_groups;
 };
 
 __host__ __device__ inline int64_t slice_at(const SliceOrder& o, int64_t x) {
@@ -35,6 +38,29 @@ __host__ __device__ inline int64_t slice_at(const SliceOrder& o, int64_t x) {
   if (x < lo) return x;
   if (x < others) return x + o.per_rank;
   return lo + (x - others);
+}
+
+// Run q of a launch over n_chunks slices x T table positions x J runs per
+// (slice, table) pair -> slice position gs (for slice_at), table position
+// tpos, run j inside the pair.  Every q in [0, n_chunks * T * J) maps to a
+// distinct triple; with table_groups G > 1, T is a multiple of G.
+__host__ __device__ inline void run_at(const SliceOrder& o, int32_t T, int32_t J, int64_t q, int64_t* gs,
+                                       int32_t* tpos, int32_t* j) {
+  if (o.table_groups == 0) {
+    const int64_t per_slice = (int64_t)T * J;
+    *gs = q / per_slice;
+    const int64_t rem = q - *gs * per_slice;
+    *tpos = (int32_t)(rem % T);
+    *j = (int32_t)(rem / T);
+    return;
+  }
+  const int64_t G = o.table_groups;
+  const int64_t per_table = o.n_chunks * J;
+  const int64_t x = q % G, i = q / G;
+  const int64_t k = i / per_table, r = i - k * per_table;
+  *tpos = (int32_t)(k * G + x);
+  *gs = r / J;
+  *j = (int32_t)(r - *gs * J);
 }
 
 struct PoolArgs {

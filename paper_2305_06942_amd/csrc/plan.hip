@@ -124,6 +124,7 @@ struct ebag_a2a_plan {
   int32_t max_ranks = 0;
   int32_t sum_dim = 0;
   int num_cus = 0;
+  int32_t table_groups = 0;  // SliceOrder::table_groups for this plan's options
   double ticks_per_us = 100.0;
   ebag_a2a_opts_t opts{};
   std::vector<TabMeta> meta;
@@ -179,6 +180,7 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
   if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
+  if (o.table_major != 0 && o.table_major != 1) return fail(EBAG_EINVAL, "table_major must be 0 or 1");
   if (o.backward_bags_per_run < 1) return fail(EBAG_EINVAL, "backward_bags_per_run must be >= 1");
   if (o.backward_waves_per_wg < 1 || o.backward_waves_per_wg > 16)
     return fail(EBAG_EINVAL, "backward_waves_per_wg must be in [1, 16]");
@@ -200,7 +202,7 @@ int check_split(const ebag_a2a_plan* h, int64_t B, int32_t R, SliceOrder* so) {
   so->per_rank = (B / R) / h->C;
   so->self = h->opts.self_rank;
   so->order = h->opts.chunk_order;
-  so->pad = 0;
+  so->table_groups = h->table_groups;
   return EBAG_OK;
 }
 
@@ -230,7 +232,7 @@ int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32
   so->per_rank = S / h->C;
   so->self = h->opts.self_rank;
   so->order = h->opts.chunk_order;
-  so->pad = 0;
+  so->table_groups = h->table_groups;
   return EBAG_OK;
 }
 
@@ -424,6 +426,8 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   // MI355X: 8 XCDs of 32 CUs.
   const int n_xcd = (h->num_cus % 32 == 0 && h->num_cus >= 64) ? h->num_cus / 32 : 1;
   std::vector<int32_t> tperm = table_order(widths, n_xcd);
+  // Table-major runs: one table group per XCD when the tables divide evenly.
+  h->table_groups = o.table_major ? (num_tables % n_xcd == 0 ? n_xcd : 1) : 0;
   CREATE_TRY(hipMalloc((void**)&h->d_meta, sizeof(TabMeta) * num_tables), "alloc table meta");
   CREATE_TRY(hipMemcpy(h->d_meta, meta.data(), sizeof(TabMeta) * num_tables, hipMemcpyHostToDevice), "upload meta");
   CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");

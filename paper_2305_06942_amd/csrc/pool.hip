@@ -469,7 +469,6 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
     __syncthreads();
   }
   const bool sc1 = FUSED && a.release_mode == 1;
-  const int64_t per_slice = (int64_t)a.T * a.J;
   const int64_t nnz = (!SAFE || a.check) ? sload(a.offsets, (int64_t)a.T * a.B) : 0;
   // One-shot grid: workgroup i pools run i.  Persistent grid (fewer
   // workgroups than runs): runs are claimed from the ticket.
@@ -477,10 +476,9 @@ __device__ __forceinline__ void pool_body(const PoolArgs& a) {
   uint32_t* s_tick = SAFE ? reinterpret_cast<uint32_t*>(lds_out) : reinterpret_cast<uint32_t*>(s_arrive + 1);
   for (int64_t q = persistent ? draw_run(a.ticket, s_tick) : (int64_t)blockIdx.x; q < a.nruns;
        q = persistent ? draw_run(a.ticket, s_tick) : a.nruns) {
-    const int64_t gs = q / per_slice;
-    const int64_t rem = q - gs * per_slice;
-    const int tpos = (int)(rem % a.T);
-    const int j = (int)(rem / a.T);
+    int64_t gs;
+    int32_t tpos, j;
+    run_at(a.so, a.T, a.J, q, &gs, &tpos, &j);
     const int t = sload(a.tperm, tpos);
     const int64_t g = slice_at(a.so, gs);
     const int64_t b0 = g * a.C + (int64_t)j * a.K;

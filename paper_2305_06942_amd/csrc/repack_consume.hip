@@ -86,8 +86,15 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
   const int64_t n_items = a.so.n_chunks * per_slice;
   const int64_t chunk_f4 = a.chunk_floats >> 2;
   for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
-    const int64_t gs = x / per_slice;
-    const int64_t p = x - gs * per_slice;
+    int64_t gs, p;
+    if (a.per_table) {  // (slice, table) items in production order
+      int32_t tp, unused;
+      run_at(a.so, a.T, 1, x, &gs, &tp, &unused);
+      p = tp;
+    } else {
+      gs = x / per_slice;
+      p = x - gs * per_slice;
+    }
     const int64_t g = slice_at(a.so, gs);
     const int t = a.per_table ? __builtin_amdgcn_readfirstlane(a.tperm[p]) : 0;
     const int64_t f = a.per_table ? g * a.T + t : g;
@@ -107,18 +114,27 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<float*>(a.send + base), 0, ((a.C - 1) * a.sum_dim + dim) * 4, kBufferWord3);
       float4* dst = reinterpret_cast<float4*>(a.recv + base);
-      for (int i0 = 0; i0 < n; i0 += 4 * 64) {
-        u4v r[4];
-        int off[4];
+      // Element e = i0 + 64 u + lane is float4 (e mod v4) of row e / v4; each
+      // lane steps its (row, column) by 64 elements at a time, so the loop
+      // divides once per item, and keeps 8 loads in flight.
+      const int drow = 64 / v4, dcol = 64 - (64 / v4) * v4;
+      int row = lane / v4, col = lane - (lane / v4) * v4;
+      for (int i0 = 0; i0 < n; i0 += 8 * 64) {
+        u4v r[8];
+        int off[8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e = i0 + u * 64 + lane;
-          const int row = e / v4;
-          off[u] = e < n ? row * ld4 + (e - row * v4) : -1;
+        for (int u = 0; u < 8; ++u) {
+          off[u] = i0 + u * 64 + lane < n ? row * ld4 + col : -1;
           r[u] = load16(rs, off[u] < 0 ? 0 : off[u] * 16, a.coherent_loads);
+          row += drow;
+          col += dcol;
+          if (col >= v4) {
+            col -= v4;
+            ++row;
+          }
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < 8; ++u)
           if (off[u] >= 0)
             dst[off[u]] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
                                       __uint_as_float(r[u].w));

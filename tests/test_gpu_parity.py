@@ -177,9 +177,11 @@ def test_full_size_sampled(name):
     configs = [dict(bench.PLAN_OPTS.get(name, {}))]
     if configs[0]:
         configs.append({})
-    send, _, flags = new_buffers(w)
+    send, _, _ = new_buffers(w)
     for opts in configs:
         plan = make_plan(w, **opts)
+        per_slice = w.T if opts.get("slice_granule") == 1 else 1
+        flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
         for fused in (True, False):
             flags.zero_()
             send.fill_(float("nan"))
@@ -187,7 +189,7 @@ def test_full_size_sampled(name):
             torch.cuda.synchronize()
             say("full", name, opts, "fused" if fused else "unfused", "ran; checking")
             assert not torch.isnan(send).any().item(), "some output element was never written"
-            assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
+            assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1, per_slice=per_slice))
             n = check_sampled(inp, send, n_bags=200)
             say("full", name, "checked", n, "bags")
         assert plan.status_ex() == (0, -1, 0, -1)

@@ -1,0 +1,22 @@
+"""The kernels' run decoding (run_at in csrc/common.h) checked on the host:
+bijective for every order, slice-major with tables fastest, table-major with
+run q in table group q mod G (no GPU; built with g++ against the HIP headers)."""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or not os.path.isdir("/opt/rocm/include"),
+                    reason="needs g++ and the HIP headers")
+def test_run_order_decoding(tmp_path):
+    exe = tmp_path / "run_order_check"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                    "-I" + os.path.join(ROOT, "paper_2305_06942_amd", "csrc"),
+                    os.path.join(ROOT, "tests", "run_order_check.cpp"), "-o", str(exe)], check=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "bad=0" in r.stdout
