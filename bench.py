@@ -55,10 +55,16 @@ def log(*a):
 
 
 def kernel_hash(kernel="fused_pool_kernel"):
+    """Hash of the kernel's sources with comments and blank space removed:
+    it changes when the code does, not when a comment does."""
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -23,9 +23,12 @@
 // checks): per-bag staging, rows stored directly, a barrier before the
 // counter update.
 //
-// Run order: runs are numbered slice-major (all runs of slice 0, then slice 1
-// ...), tables fastest inside a slice, so slices complete progressively and a
-// consumer can drain them while later slices are still being pooled.
+// Run order (run_at): by default runs are numbered slice-major (all runs of
+// slice 0, then slice 1 ...), tables fastest inside a slice, so slices
+// complete progressively and a consumer can drain them while later slices
+// are still being pooled.  Table-major order pools one table at a time per
+// XCD (its hot rows stay cached); with per-table slices those still complete
+// progressively.
 #include "common.h"
 
 namespace ebag {
