@@ -28,8 +28,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, public specification
 # Sources whose text fixes each profiled kernel: committed counter records
 # are used only while the hash of these files is unchanged.
 KERNEL_SOURCES = {
-    "fused_pool_kernel": ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h",
-                          "paper_2305_06942_amd/csrc/repack_consume.hip"],
+    "fused_pool_kernel": ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h"],
     "backward_kernel": ["paper_2305_06942_amd/csrc/backward.hip", "paper_2305_06942_amd/csrc/backward.h",
                         "paper_2305_06942_amd/csrc/common.h"],
 }

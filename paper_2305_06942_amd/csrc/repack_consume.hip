@@ -64,8 +64,8 @@ __device__ __forceinline__ uint32_t wait_flag(const ConsumeArgs& a, int64_t f, u
 }
 
 __device__ __forceinline__ u4v load16(__amdgpu_buffer_rsrc_t rs, int off, bool coherent) {
-  return coherent ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16)
-                  : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+  return coherent ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 18)
+                  : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 2);
 }
 
 // Receiver (Sec. III-A, "Book-keeping Flags").  Single-wave workgroups take
@@ -136,8 +136,7 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u)
           if (off[u] >= 0)
-            dst[off[u]] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
-                                      __uint_as_float(r[u].w));
+            __builtin_nontemporal_store(r[u], reinterpret_cast<u4v*>(dst) + off[u]);
       }
     } else {
       const int64_t e0 = p * a.piece_f4;
@@ -153,8 +152,7 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           const int i = i0 + u * 64 + lane;
-          if (i < n) dst[i] = make_float4(__uint_as_float(r[u].x), __uint_as_float(r[u].y), __uint_as_float(r[u].z),
-                                          __uint_as_float(r[u].w));
+          if (i < n) __builtin_nontemporal_store(r[u], reinterpret_cast<u4v*>(dst) + i);
         }
       }
     }
