@@ -3,7 +3,7 @@
 Each case draws a storage type, per-table widths (16-byte multiples, some not
 a power of two in 16-byte vectors), table sizes, batch split (B, R, C), bag
 length law (with empty and long bags), weights or mean pooling, slice
-granule, slice order and launch options, then checks the fused and unfused
+granule, slice and run order and launch options, then checks the fused and unfused
 results element by element, the flags, and the consumer's copy."""
 import dataclasses
 
@@ -17,7 +17,7 @@ from tests.gpu_util import check_full, flags_np, make_plan, run, say
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 64
+N_CASES = 96
 _QUEUE = []
 
 
@@ -79,6 +79,7 @@ def _case(seed):
                 waves_per_wg=int(rng.choice([1, 2, 4, 8])), bags_per_run=int(rng.choice([1, 3, 16, 40])),
                 rows_in_flight=int(rng.choice([4, 8])), persistent_wgs_per_cu=int(rng.choice([0, 0, 1, 3])),
                 check_indices=int(rng.integers(0, 2)), stream_rows=int(rng.integers(0, 2)))
+    opts["table_major"] = int(rng.integers(0, 2))
     return inp, opts
 
 
