@@ -40,10 +40,13 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    tables) with the paper's per-table slices (slice_granule = 1), so a
 #    table's hot rows stay cached while it is pooled;
 #  * mixed has many short runs (64-byte rows, variable lengths): a persistent
-#    grid claiming runs from the ticket beats one workgroup per run there.
-PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1},
-             "large": {"stream_rows": 0, "table_major": 1, "slice_granule": 1},
-             "mixed": {"persistent_wgs_per_cu": -1}}
+#    grid claiming runs from the ticket beats one workgroup per run there;
+#  * where rows are reused (skewed, large, mixed's small tables) the consumer
+#    copies non-temporally (consume_nontemporal = 1), so its stream does not
+#    displace the producer's cached rows; on dlrm plain copies are faster.
+PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
+             "large": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
+             "mixed": {"persistent_wgs_per_cu": -1, "consume_nontemporal": 1}}
 PAPER_CONTEXT = ("the paper's fused embedding + All-to-All reduced execution time by 20% intra-node "
                  "(4x MI210 over Infinity Fabric, 80 GB/s) and 31% inter-node (2x MI210 over InfiniBand, "
                  "20 GB/s); context only, those numbers include real inter-GPU transport")

@@ -119,6 +119,10 @@ typedef struct ebag_a2a_opts {
                                   slice_granule = 1, whose per-table slices then still complete
                                   progressively; with whole slices every slice completes at the end.  The
                                   consumer, backward and delivery follow the same order. */
+  int32_t consume_nontemporal; /* 1: the consumer reads and writes slice data non-temporally, so its
+                                  stream does not displace the producer's cached table rows (pays off
+                                  when rows are reused: Zipf indices, small tables); 0 (default): plain
+                                  loads and stores, which may hit the freshly written slices in cache */
 } ebag_a2a_opts_t;
 
 /* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */

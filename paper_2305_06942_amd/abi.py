@@ -38,6 +38,7 @@ class Opts(ctypes.Structure):
         ("backward_bags_per_run", ctypes.c_int32),
         ("backward_waves_per_wg", ctypes.c_int32),
         ("table_major", ctypes.c_int32),
+        ("consume_nontemporal", ctypes.c_int32),
     ]
 
 

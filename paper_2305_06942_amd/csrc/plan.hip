@@ -12,6 +12,7 @@
 #include "ebag_a2a.h"
 #include "common.h"
 #include "backward.h"
+#include "consume.h"
 
 using namespace ebag;
 
@@ -181,6 +182,8 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
   if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
   if (o.table_major != 0 && o.table_major != 1) return fail(EBAG_EINVAL, "table_major must be 0 or 1");
+  if (o.consume_nontemporal != 0 && o.consume_nontemporal != 1)
+    return fail(EBAG_EINVAL, "consume_nontemporal must be 0 or 1");
   if (o.backward_bags_per_run < 1) return fail(EBAG_EINVAL, "backward_bags_per_run must be >= 1");
   if (o.backward_waves_per_wg < 1 || o.backward_waves_per_wg > 16)
     return fail(EBAG_EINVAL, "backward_waves_per_wg must be in [1, 16]");
@@ -541,6 +544,7 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   c.so.order = h->opts.chunk_order;
   c.epoch = expected_epoch;
   c.coherent_loads = h->opts.release_mode == 1;
+  c.nontemporal = h->opts.consume_nontemporal;
   c.per_table = h->opts.slice_granule == 1;
   c.meta = h->d_meta;
   c.tperm = h->d_tperm;

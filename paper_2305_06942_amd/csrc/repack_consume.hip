@@ -1,5 +1,5 @@
 // Repack kernel of the unfused baseline and the flag-polling consumer.
-#include "common.h"
+#include "consume.h"
 
 namespace ebag {
 namespace {
@@ -63,9 +63,18 @@ __device__ __forceinline__ uint32_t wait_flag(const ConsumeArgs& a, int64_t f, u
   return v;
 }
 
-__device__ __forceinline__ u4v load16(__amdgpu_buffer_rsrc_t rs, int off, bool coherent) {
-  return coherent ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 18)
-                  : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 2);
+// Cache policy bits of a buffer load: 16 = sc1 (device scope), 2 = nt.
+__device__ __forceinline__ u4v load16(__amdgpu_buffer_rsrc_t rs, int off, bool coherent, bool nt) {
+  if (coherent) return nt ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 18)
+                          : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 16);
+  return nt ? __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 2) : __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+}
+
+__device__ __forceinline__ void store16(u4v* p, const u4v& v, bool nt) {
+  if (nt)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
 }
 
 // Receiver (Sec. III-A, "Book-keeping Flags").  Single-wave workgroups take
@@ -125,7 +134,7 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           off[u] = i0 + u * 64 + lane < n ? row * ld4 + col : -1;
-          r[u] = load16(rs, off[u] < 0 ? 0 : off[u] * 16, a.coherent_loads);
+          r[u] = load16(rs, off[u] < 0 ? 0 : off[u] * 16, a.coherent_loads, a.nontemporal);
           row += drow;
           col += dcol;
           if (col >= v4) {
@@ -136,7 +145,7 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u)
           if (off[u] >= 0)
-            __builtin_nontemporal_store(r[u], reinterpret_cast<u4v*>(dst) + off[u]);
+            store16(reinterpret_cast<u4v*>(dst) + off[u], r[u], a.nontemporal);
       }
     } else {
       const int64_t e0 = p * a.piece_f4;
@@ -148,11 +157,11 @@ __global__ __launch_bounds__(64) void consume_kernel(const ConsumeArgs a) {
       for (int i0 = 0; i0 < n; i0 += 8 * 64) {
         u4v r[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) r[u] = load16(rs, (i0 + u * 64 + lane) * 16, a.coherent_loads);
+        for (int u = 0; u < 8; ++u) r[u] = load16(rs, (i0 + u * 64 + lane) * 16, a.coherent_loads, a.nontemporal);
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
           const int i = i0 + u * 64 + lane;
-          if (i < n) __builtin_nontemporal_store(r[u], reinterpret_cast<u4v*>(dst) + i);
+          if (i < n) store16(reinterpret_cast<u4v*>(dst) + i, r[u], a.nontemporal);
         }
       }
     }

@@ -182,9 +182,10 @@ def test_bad_index_reported_and_skipped():
     assert np.all(flags_np(flags) == 1)
 
 
-@pytest.mark.parametrize("opts", [dict(), dict(slice_granule=1), dict(persistent_wgs_per_cu=-1, chunk_order=1,
-                                                                      self_rank=3)],
-                         ids=["default", "per_table", "persistent_comm_aware"])
+@pytest.mark.parametrize("opts", [dict(), dict(slice_granule=1, consume_nontemporal=1),
+                                  dict(persistent_wgs_per_cu=-1, chunk_order=1, self_rank=3),
+                                  dict(table_major=1, slice_granule=1, consume_nontemporal=1, release_mode=0)],
+                         ids=["default", "per_table_nt", "persistent_comm_aware", "table_major_nt_release0"])
 def test_stress_100_epochs_across_flag_wraparound(opts):
     """100 forwards, each drained concurrently by the consumer, with the epoch
     flags starting 50 below 2^32 so that they wrap to 0 midway: every epoch

@@ -80,6 +80,7 @@ def _case(seed):
                 rows_in_flight=int(rng.choice([4, 8])), persistent_wgs_per_cu=int(rng.choice([0, 0, 1, 3])),
                 check_indices=int(rng.integers(0, 2)), stream_rows=int(rng.integers(0, 2)))
     opts["table_major"] = int(rng.integers(0, 2))
+    opts["consume_nontemporal"] = int(rng.integers(0, 2))
     return inp, opts
 
 
