@@ -95,3 +95,37 @@ def sample_bags(w, n, seed=0):
     while len(bags) < n:
         bags.add((int(rng.integers(0, w.T)), int(rng.integers(0, w.B))))
     return sorted(bags)
+
+
+def backward_bag(inputs, grad, t, b, mean=False):
+    """Per-lookup gradient rows of bag (t, b), fp32 [L, D_t]: lookup k gets
+    w_k * g (sum and weighted sum; w_k = 1 without weights) or g / L (mean),
+    g = grad[b, off_t : off_t + D_t] -- the derivative of the pooled value
+    with respect to each gathered row (Sec. III-A pooling, run backwards as
+    in the training pass of Sec. IV-D), each value one fp32 operation."""
+    w = inputs.w
+    lo, hi = int(inputs.offsets[t * w.B + b]), int(inputs.offsets[t * w.B + b + 1])
+    D = w.dims[t]
+    col = int(column_offsets(w.dims)[t])
+    g = np.asarray(grad[b, col:col + D], dtype=np.float32)
+    L = hi - lo
+    rows = np.empty((L, D), dtype=np.float32)
+    for k in range(L):
+        if mean:
+            rows[k] = g / np.float32(L)
+        elif inputs.weights is not None:
+            rows[k] = np.float32(inputs.weights[lo + k]) * g
+        else:
+            rows[k] = g
+    return rows
+
+
+def backward_value_offset(inputs, t, b):
+    """First value of bag (t, b) in the backward's output: the table blocks
+    (nnz_t x D_t values each) follow each other in table order, lookups in
+    order inside a block."""
+    w = inputs.w
+    base = 0
+    for u in range(t):
+        base += int(inputs.offsets[(u + 1) * w.B] - inputs.offsets[u * w.B]) * w.dims[u]
+    return base + int(inputs.offsets[t * w.B + b] - inputs.offsets[t * w.B]) * w.dims[t]

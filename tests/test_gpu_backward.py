@@ -188,3 +188,41 @@ def test_backward_full_size_dlrm_fused():
     _check(inp, grad_dp, values, False)
     del values
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["skewed", "large", "mixed"])
+def test_backward_full_size_sampled(name):
+    """Full workload sizes in the launch configuration the backward benchmark
+    times (the workload's plan options without the row-cache and grid ones),
+    fused with the delivery: sampled bags bit for bit against the per-bag
+    oracle, every flag, and no value left unwritten."""
+    import torch
+    import bench
+    from oracle import sampled
+    w = synth.FULL[name]
+    say("backward full", name)
+    inp = synth.make_inputs(w)
+    opts = {k: v for k, v in bench.PLAN_OPTS.get(name, {}).items()
+            if k not in ("stream_rows", "persistent_wgs_per_cu")}
+    plan = make_plan(w, **opts)
+    offsets = torch.from_numpy(inp.offsets).cuda()
+    weights = None if inp.weights is None else torch.from_numpy(inp.weights).cuda()
+    dev = sdev.DeviceInputs(None, None, offsets, weights)
+    flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
+    grad_recv = torch.empty((w.B, w.sum_dim), device="cuda")
+    grad_dp = _grad(w, 9)
+    n = _n_values(inp)
+    say("backward full", name, "values", n)
+    values = torch.full((n,), float("nan"), device="cuda")
+    _fused(plan, w, dev, grad_dp, grad_recv, flags, values, 1)
+    assert plan.status_ex() == (0, -1, 0, -1)
+    assert np.all(flags.cpu().numpy() == 1)
+    assert not torch.isnan(values).any().item(), "some value was never written"
+    g = grad_dp.cpu().numpy()
+    for t, b in sampled.sample_bags(w, 300, seed=5):
+        want = sampled.backward_bag(inp, g, t, b)
+        o = sampled.backward_value_offset(inp, t, b)
+        got = values[o:o + want.size].cpu().numpy()
+        assert np.array_equal(got.view(np.uint32), want.reshape(-1).view(np.uint32)), f"bag (t={t}, b={b})"
+    del values, grad_recv
+    torch.cuda.empty_cache()

@@ -73,3 +73,19 @@ def test_flags_shape():
     assert f.shape == (64,) and np.all(f == 5)
     with pytest.raises(oracle.OracleError):
         oracle.flags(4096, 8, 100, 1)
+
+
+@pytest.mark.parametrize("base", [DLRM, SKEWED, LARGE, MIXED], ids=lambda w: w.name)
+def test_sampled_backward_matches_c(oracle_lib, base):
+    """The numpy per-bag backward (values and their position) and the C
+    oracle's whole backward agree bit for bit on small versions of every
+    workload, for sum / weighted sum and mean."""
+    w = scaled(base, rows=300, B=base.R * base.C, T=min(base.T, 8))
+    inp = make_inputs(w)
+    grad = np.random.default_rng(3).standard_normal((w.B, w.sum_dim)).astype(np.float32)
+    for mean in ((False, True) if inp.weights is None else (False,)):
+        full = oracle.backward(w.dims, inp.offsets, inp.weights, grad, w.B, w.R, mean=mean, lib=oracle_lib)
+        for t, b in sampled.sample_bags(w, 60, seed=1):
+            want = sampled.backward_bag(inp, grad, t, b, mean=mean).reshape(-1)
+            o = sampled.backward_value_offset(inp, t, b)
+            assert np.array_equal(full[o:o + want.size].view(np.uint32), want.view(np.uint32)), (t, b, mean)
