@@ -373,6 +373,9 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
     tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
     e2e_us(tplan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, 0)
     rel, drn, tpu = tplan.trace(n_flags)
+    tplan.close()
+    for q in (prod, cons):
+        ebag.queue_stream_destroy(q)
     out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
     out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
     out["median_drain_lag_us"] = round(float(np.median(drn.astype(np.int64) - rel.astype(np.int64))) / tpu, 2)
@@ -526,6 +529,8 @@ def run_timeline(name, warmup):
         plan.close()
         out.append(row)
         print(json.dumps(row), flush=True)
+    for q in (prod, cons):
+        ebag.queue_stream_destroy(q)
     return out
 
 
@@ -646,6 +651,8 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
     row["env"] = env_info(inp)
     print(json.dumps(row), flush=True)
     plan.close()
+    for q in (send_q, bwd_q):
+        ebag.queue_stream_destroy(q)
     return row
 
 
@@ -744,19 +751,24 @@ def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
     return out
 
 
-def summarize(d):
+def summarize(d, dispatches=None):
     """Summarise rocprofv3 csv output under d: per-kernel dispatch count and
-    mean / median duration, and per-kernel mean counter values."""
+    mean / median duration, and per-kernel mean counter values.  dispatches
+    "A:B" keeps each kernel's dispatches A..B (1-based, in start order) --
+    e.g. the timed region of a bench run after its warm-up launches."""
     import csv
     import statistics
     lines = []
+    lo, hi = (int(x) for x in dispatches.split(":")) if dispatches else (1, None)
     for path in sorted(glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)):
         per = {}
         with open(path) as f:
-            for r in csv.DictReader(f):
-                dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
-                per.setdefault(r["Kernel_Name"], []).append(dur)
-        lines.append(f"# kernel trace: {os.path.relpath(path, d)}")
+            recs = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
+        for r in recs:
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            per.setdefault(r["Kernel_Name"], []).append(dur)
+        per = {k: v[lo - 1:hi] for k, v in per.items() if v[lo - 1:hi]}
+        lines.append(f"# kernel trace: {os.path.relpath(path, d)}" + (f" (dispatches {dispatches} of each kernel)" if dispatches else ""))
         lines.append(f"{'kernel':60s} {'calls':>6s} {'mean_us':>10s} {'median_us':>10s} {'min_us':>10s}")
         for k, v in sorted(per.items(), key=lambda kv: -sum(kv[1])):
             lines.append(f"{k[:60]:60s} {len(v):6d} {statistics.mean(v):10.2f} {statistics.median(v):10.2f} "
@@ -817,6 +829,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile", action="store_true", help="timing loops only (for rocprofv3 runs)")
     ap.add_argument("--summarize", metavar="DIR")
+    ap.add_argument("--dispatches", metavar="A:B", help="with --summarize: each kernel's dispatches A..B only")
     ap.add_argument("--traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     ap.add_argument("--occupancy", action="store_true", help="persistent-grid occupancy sweep of the fused kernel")
     ap.add_argument("--timeline", action="store_true", help="per-slice release / drain times, both slice orders")
@@ -830,7 +843,7 @@ def main():
     ap.add_argument("--stream-probe", action="store_true", help="streaming read and write ceilings")
     a = ap.parse_args()
     if a.summarize:
-        print(summarize(a.summarize))
+        print(summarize(a.summarize, a.dispatches))
         return 0
     if a.traffic:
         kernel = "backward_kernel" if a.backward else "fused_pool_kernel"

@@ -277,9 +277,14 @@ int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]);
  * with every CU enabled), for running ebag_a2a_consume concurrently with a
  * forward: ordinary streams of a process share a few hardware queues, and
  * two kernels on one queue run one after the other.  Release it with
- * hipStreamDestroy.
+ * ebag_a2a_queue_stream_destroy (or hipStreamDestroy).
  */
 int ebag_a2a_queue_stream_create(hipStream_t* out);
+
+/* Wait for a stream from ebag_a2a_queue_stream_create to drain, then destroy
+ * it (its hardware queue is released).  Returns EBAG_OK, EBAG_EINVAL (null
+ * stream) or EBAG_EHIP. */
+int ebag_a2a_queue_stream_destroy(hipStream_t stream);
 
 /* Release the plan's device memory.  NULL is ignored. */
 void ebag_a2a_destroy(ebag_a2a_t h);

@@ -78,6 +78,7 @@ _SIGS = {
     "ebag_a2a_trace": ([_P, _P, _P, ctypes.c_int64, _P], ctypes.c_int),
     "ebag_a2a_occupancy": ([_P, ctypes.c_int32, _P], ctypes.c_int),
     "ebag_a2a_queue_stream_create": ([_P], ctypes.c_int),
+    "ebag_a2a_queue_stream_destroy": ([_P], ctypes.c_int),
     "ebag_a2a_destroy": ([_P], None),
     "ebag_a2a_last_error": ([], ctypes.c_char_p),
     "gemv_ar_default_opts": ([_P], ctypes.c_int),
@@ -152,6 +153,11 @@ def queue_stream():
     s = ctypes.c_void_p()
     _check(load().ebag_a2a_queue_stream_create(ctypes.byref(s)))
     return torch.cuda.ExternalStream(s.value)
+
+
+def queue_stream_destroy(stream):
+    """Drain and destroy a stream from queue_stream() (ebag_a2a_queue_stream_destroy)."""
+    _check(load().ebag_a2a_queue_stream_destroy(_stream(stream)))
 
 
 def default_opts() -> Opts:

@@ -731,6 +731,13 @@ int ebag_a2a_queue_stream_create(hipStream_t* out) {
   return EBAG_OK;
 }
 
+int ebag_a2a_queue_stream_destroy(hipStream_t stream) {
+  if (!stream) return fail(EBAG_EINVAL, "null stream");
+  HIP_TRY(hipStreamSynchronize(stream), "synchronize stream");
+  HIP_TRY(hipStreamDestroy(stream), "destroy stream");
+  return EBAG_OK;
+}
+
 void ebag_a2a_destroy(ebag_a2a_t h) { free_plan(h); }
 
 const char* ebag_a2a_last_error(void) { return g_err.c_str(); }
