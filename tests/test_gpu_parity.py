@@ -174,11 +174,11 @@ def test_full_size_sampled(name):
     inp = synth.make_inputs(w)
     say("full", name, "nnz", inp.nnz, "to device")
     dev = sdev.to_device(inp)
-    configs = [dict(bench.PLAN_OPTS.get(name, {}))]
-    if configs[0]:
-        configs.append({})
+    launches = [dict(bench.PLAN_OPTS.get(name, {}))]
+    if launches[0]:
+        launches.append({})
     send, _, _ = new_buffers(w)
-    for opts in configs:
+    for opts in launches:
         plan = make_plan(w, **opts)
         per_slice = w.T if opts.get("slice_granule") == 1 else 1
         flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
