@@ -153,3 +153,22 @@ def test_gemv_ar_suppressed_peer_flag_times_out():
         got = y[r].cpu().numpy()
         assert np.all(np.isnan(got[missing]))
         assert np.all(np.abs(got[~missing] - y64[~missing]) <= rel * abs64[~missing] + 1e-30)
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_gemv_ar_random(seed):
+    """Seeded random shapes and launches: ranks 1..16, ragged M, per-rank K
+    (16-byte multiples, up to the 64 KiB LDS limit), every storage type,
+    integer or normal values, tile height, waves, workgroups per rank, order
+    and reduction mode; two epochs each, fused and unfused."""
+    rng = np.random.default_rng([2305, 6942, 5, seed])
+    dtype = int(rng.integers(0, 3))
+    elt = 4 if dtype == synth.F32 else 2
+    R = int(rng.choice([1, 2, 3, 4, 7, 8, 16]))
+    M = int(rng.integers(1, 5000))
+    Ks = [(16 // elt) * int(rng.integers(1, 300)) for _ in range(R)]
+    opts = dict(tile_rows=int(rng.choice([0, 1, 7, 32, 64, 128, 300])), waves_per_wg=int(rng.choice([1, 2, 4, 16])),
+                comm_aware=int(rng.integers(0, 2)), reduce_mode=int(rng.integers(0, 2)))
+    if rng.random() < 0.3:
+        opts["wgs_per_rank"] = int(rng.integers(1, 9))
+    _run(R, M, Ks, dtype, seed=1000 + seed, integer=bool(rng.integers(0, 2)), **opts)
