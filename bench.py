@@ -34,19 +34,20 @@ KERNEL_SOURCES = {
 }
 TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json"}
 # Launch options per workload (every other option at its default):
-#  * Zipf-distributed indices reuse hot rows, so the Zipf workloads read rows
-#    through the caches (stream_rows = 0) rather than streaming them, and go
-#    table by table (table_major = 1, each XCD working through its own
-#    tables) with the paper's per-table slices (slice_granule = 1), so a
-#    table's hot rows stay cached while it is pooled;
-#  * mixed has many short runs (64-byte rows, variable lengths): a persistent
-#    grid claiming runs from the ticket beats one workgroup per run there;
-#  * where rows are reused (skewed, large, mixed's small tables) the consumer
-#    copies non-temporally (consume_nontemporal = 1), so its stream does not
-#    displace the producer's cached rows; on dlrm plain copies are faster.
+#  * where rows are reused -- Zipf indices (skewed, large), or tables small
+#    enough for the Infinity Cache (mixed's 64-256 MB tables) -- rows are
+#    read through the caches (stream_rows = 0) and pooled table by table with
+#    the paper's per-table slices (slice_granule = 1), so a table's rows stay
+#    cached while it is pooled: skewed with one table per XCD at a time
+#    (table_major = 1, its hot rows fit an XCD's L2), large and mixed with
+#    one table at a time for the whole device (table_major = 2, the table's
+#    working set shares the device-wide cache);
+#  * there the consumer copies non-temporally (consume_nontemporal = 1), so
+#    its stream does not displace the producer's cached rows; dlrm streams
+#    its rows and keeps the defaults.
 PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
-             "large": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
-             "mixed": {"persistent_wgs_per_cu": -1, "consume_nontemporal": 1}}
+             "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1},
+             "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1}}
 PAPER_CONTEXT = ("the paper's fused embedding + All-to-All reduced execution time by 20% intra-node "
                  "(4x MI210 over Infinity Fabric, 80 GB/s) and 31% inter-node (2x MI210 over InfiniBand, "
                  "20 GB/s); context only, those numbers include real inter-GPU transport")
@@ -90,7 +91,7 @@ def traffic_record(workload, kernel="fused_pool_kernel"):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_hash") != kernel_hash(kernel):
+    if rec.get("kernel_hash") != kernel_hash(kernel) or rec.get("plan_options") != PLAN_OPTS.get(workload, {}):
         return None
     return rec
 
@@ -814,6 +815,7 @@ def traffic(fetch_dir, write_dir, workload, kernel="fused_pool_kernel", calib="c
     fetch_b = fe[kf] * f_scale * 1024
     write_b = wr[kw] * w_scale * 1024
     return {"workload": workload, "kernel": kernel, "kernel_hash": kernel_hash(kernel),
+            "plan_options": PLAN_OPTS.get(workload, {}),
             "fetch_kib_raw": fe[kf], "write_kib_raw": wr[kw], "fetch_scale": round(f_scale, 4),
             "write_scale": round(w_scale, 4), "fetch_bytes": int(fetch_b), "write_bytes": int(write_b),
             "hbm_bytes_per_launch": int(fetch_b + write_b)}

@@ -115,10 +115,11 @@ typedef struct ebag_a2a_opts {
   int32_t table_major;         /* 0 (default): runs slice by slice, tables fastest inside a slice; 1: table
                                   by table, slices in order inside each table, and (when T is a multiple
                                   of the XCD count) each XCD working through its own tables one at a time,
-                                  so that a table's hot rows stay in that XCD's caches.  Meant for
-                                  slice_granule = 1, whose per-table slices then still complete
-                                  progressively; with whole slices every slice completes at the end.  The
-                                  consumer, backward and delivery follow the same order. */
+                                  so that a table's hot rows stay in that XCD's caches; 2: table by table
+                                  for the whole device, so that one table's rows share the device-wide
+                                  cache.  Meant for slice_granule = 1, whose per-table slices then still
+                                  complete progressively; with whole slices every slice completes at the
+                                  end.  The consumer, backward and delivery follow the same order. */
   int32_t consume_nontemporal; /* 1: the consumer reads and writes slice data non-temporally, so its
                                   stream does not displace the producer's cached table rows (pays off
                                   when rows are reused: Zipf indices, small tables); 0 (default): plain

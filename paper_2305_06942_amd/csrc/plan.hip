@@ -181,7 +181,7 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.consume_timeout_us < 1) return fail(EBAG_EINVAL, "consume_timeout_us must be >= 1");
   if (o.pooling_mode != 0 && o.pooling_mode != 1) return fail(EBAG_EINVAL, "pooling_mode must be 0 (sum) or 1 (mean)");
   if (o.slice_granule != 0 && o.slice_granule != 1) return fail(EBAG_EINVAL, "slice_granule must be 0 or 1");
-  if (o.table_major != 0 && o.table_major != 1) return fail(EBAG_EINVAL, "table_major must be 0 or 1");
+  if (o.table_major < 0 || o.table_major > 2) return fail(EBAG_EINVAL, "table_major must be 0, 1 or 2");
   if (o.consume_nontemporal != 0 && o.consume_nontemporal != 1)
     return fail(EBAG_EINVAL, "consume_nontemporal must be 0 or 1");
   if (o.backward_bags_per_run < 1) return fail(EBAG_EINVAL, "backward_bags_per_run must be >= 1");
@@ -429,8 +429,10 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   // MI355X: 8 XCDs of 32 CUs.
   const int n_xcd = (h->num_cus % 32 == 0 && h->num_cus >= 64) ? h->num_cus / 32 : 1;
   std::vector<int32_t> tperm = table_order(widths, n_xcd);
-  // Table-major runs: one table group per XCD when the tables divide evenly.
-  h->table_groups = o.table_major ? (num_tables % n_xcd == 0 ? n_xcd : 1) : 0;
+  // Table-major runs: 1 -> one table group per XCD when the tables divide
+  // evenly (each XCD pools its own tables); 2 -> one table at a time for the
+  // whole device.
+  h->table_groups = o.table_major == 2 ? 1 : o.table_major == 1 ? (num_tables % n_xcd == 0 ? n_xcd : 1) : 0;
   CREATE_TRY(hipMalloc((void**)&h->d_meta, sizeof(TabMeta) * num_tables), "alloc table meta");
   CREATE_TRY(hipMemcpy(h->d_meta, meta.data(), sizeof(TabMeta) * num_tables, hipMemcpyHostToDevice), "upload meta");
   CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");

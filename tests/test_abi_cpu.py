@@ -77,7 +77,7 @@ def test_create_rejects(lib, kw, msg):
     ("rows_in_flight", 5, "rows_in_flight"), ("bags_per_run", 0, "bags_per_run"),
     ("chunk_order", 2, "chunk_order"), ("consumer_wgs", 0, "consumer_wgs"),
     ("backward_bags_per_run", 0, "backward_bags_per_run"), ("backward_waves_per_wg", 17, "backward_waves_per_wg"),
-    ("table_major", 2, "table_major"), ("consume_nontemporal", 3, "consume_nontemporal"),
+    ("table_major", 3, "table_major"), ("table_major", -1, "table_major"), ("consume_nontemporal", 3, "consume_nontemporal"),
 ])
 def test_create_rejects_opts(lib, field, value, msg):
     import paper_2305_06942_amd as ebag

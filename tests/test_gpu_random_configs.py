@@ -79,7 +79,7 @@ def _case(seed):
                 waves_per_wg=int(rng.choice([1, 2, 4, 8])), bags_per_run=int(rng.choice([1, 3, 16, 40])),
                 rows_in_flight=int(rng.choice([4, 8])), persistent_wgs_per_cu=int(rng.choice([0, 0, 1, 3])),
                 check_indices=int(rng.integers(0, 2)), stream_rows=int(rng.integers(0, 2)))
-    opts["table_major"] = int(rng.integers(0, 2))
+    opts["table_major"] = int(rng.integers(0, 3))
     opts["consume_nontemporal"] = int(rng.integers(0, 2))
     return inp, opts
 

@@ -31,17 +31,18 @@ def _cuda():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("major", [1, 2], ids=["per_xcd", "device"])
 @pytest.mark.parametrize("persistent", [0, -1], ids=["one_shot", "persistent"])
 @pytest.mark.parametrize("granule", [0, 1])
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
-def test_table_major_parity(name, granule, persistent):
+def test_table_major_parity(name, granule, persistent, major):
     import torch
     w = WORKLOADS[name]
-    say("table-major", name, granule, persistent)
+    say("table-major", name, granule, persistent, major)
     inp = synth.make_inputs(w)
     dev = sdev.to_device(inp)
     s64, a64, _ = oracle.pool_inputs(inp)
-    plan = make_plan(w, table_major=1, slice_granule=granule, persistent_wgs_per_cu=persistent)
+    plan = make_plan(w, table_major=major, slice_granule=granule, persistent_wgs_per_cu=persistent)
     per_slice = w.T if granule else 1
     outs = []
     for fused in (True, False):
@@ -57,8 +58,9 @@ def test_table_major_parity(name, granule, persistent):
     assert plan.status_ex() == (0, -1, 0, -1)
 
 
+@pytest.mark.parametrize("major", [1, 2], ids=["per_xcd", "device"])
 @pytest.mark.parametrize("name", ["skewed_t16", "mixed_small"])
-def test_table_major_consumer_and_backward(name):
+def test_table_major_consumer_and_backward(name, major):
     """Consumer drains per-table slices in table-major order; the backward
     expands the gradient as the delivery (same order) lands; three epochs."""
     import torch
@@ -66,7 +68,7 @@ def test_table_major_consumer_and_backward(name):
     w = WORKLOADS[name]
     inp = synth.make_inputs(w)
     dev = sdev.to_device(inp)
-    plan = make_plan(w, table_major=1, slice_granule=1, chunk_order=1, self_rank=1)
+    plan = make_plan(w, table_major=major, slice_granule=1, chunk_order=1, self_rank=1)
     send, recv, _ = new_buffers(w)
     flags = torch.zeros(w.n_chunks * w.T, dtype=torch.int32, device="cuda")
     gflags = torch.zeros_like(flags)
