@@ -342,7 +342,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
                    "bag_lengths": w.lengths, "indices": w.indices, "weighted": w.weighted,
                    "pooling": "mean" if mean else "sum",
                    "slices": "per table" if per_table_slices else "all tables",
-                   "run_order": "table-major" if opts.get("table_major") else "slice-major",
+                   "run_order": {0: "slice-major", 1: "table-major, one table per XCD at a time",
+                                 2: "table-major, one table at a time"}[opts.get("table_major", 0)],
                    "destinations": w.R, "slice_samples": w.C, "parallelism": "1 GPU, R logical destinations"},
         "fused_us": round(fused_ms * 1e3, 2),
         "unfused_us": round(unfused_ms * 1e3, 2),
