@@ -81,6 +81,7 @@ def _case(seed):
                 check_indices=int(rng.integers(0, 2)), stream_rows=int(rng.integers(0, 2)))
     opts["table_major"] = int(rng.integers(0, 3))
     opts["consume_nontemporal"] = int(rng.integers(0, 2))
+    opts["release_mode"] = int(rng.random() < 0.25)
     return inp, opts
 
 
