@@ -47,7 +47,9 @@
  *  n forwards every flag equals n.
  *
  *  Pointers named *_buf, tables, indices, offsets, weights and flags are
- *  device pointers owned by the caller; the library never frees them.  All
+ *  device pointers owned by the caller; the library never frees them.
+ *  indices must be non-null even when every bag is empty (nnz = 0): the
+ *  library cannot read nnz on the host, and never reads past offsets.  All
  *  device work is enqueued on the given HIP stream; calls return as soon as
  *  the work is enqueued.  One forward (fused or unfused) may be in flight per
  *  plan at a time: the plan's slice counters and unfused scratch are shared.

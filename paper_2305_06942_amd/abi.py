@@ -189,6 +189,18 @@ class Plan:
         self._h = h
         self._lib = lib
         self._tab_cache = None
+        self._empty_idx = None
+
+    def _indices(self, indices):
+        """An empty index tensor (every bag empty) has no device address; the
+        C ABI takes a valid pointer that is never read, so pass a one-element
+        device buffer instead."""
+        if hasattr(indices, "numel") and indices.numel() == 0:
+            if self._empty_idx is None or self._empty_idx.device != indices.device:
+                import torch
+                self._empty_idx = torch.zeros(1, dtype=torch.int32, device=indices.device)
+            return self._empty_idx.data_ptr()
+        return _addr(indices)
 
     def _tables(self, tables):
         ptrs = [_addr(t) for t in tables]
@@ -204,12 +216,12 @@ class Plan:
 
     def forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
-        _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
+        _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), self._indices(indices), _addr(offsets),
                                           _addr(weights), int(B), int(R), _addr(send), _addr(flags), _stream(stream)))
 
     def unfused_forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
-        _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), _addr(indices), _addr(offsets),
+        _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), self._indices(indices), _addr(offsets),
                                                   _addr(weights), int(B), int(R), _addr(send), _addr(flags),
                                                   _stream(stream)))
 

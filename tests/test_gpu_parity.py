@@ -141,6 +141,7 @@ EDGE = {
     "wide_rows_512": (synth.F32, [512, 1024], [20, 10], 8, 2, 2, lambda r, n: r.integers(1, 40, n), False),
     "fp16_wide_ragged": (synth.F16, [8, 24, 256, 72], [100, 7, 60, 9], 12, 3, 2, lambda r, n: r.integers(0, 70, n), True),
     "many_tables": (synth.BF16, [32] * 70, [64] * 70, 4, 2, 1, lambda r, n: r.integers(1, 9, n), False),
+    "all_bags_empty": (synth.F16, [64, 32], [50, 40], 8, 2, 2, lambda r, n: np.zeros(n, dtype=np.int64), True),
 }
 
 
