@@ -176,6 +176,40 @@ def probe_ceiling(w, lengths, weighted, nt):
     return alg / (us * 1e-6) / 1e9, us
 
 
+def run_torch_baseline(name, steps, warmup):
+    """PyTorch's own path for the same operation, as a framework user would
+    write it: one torch.nn.functional.embedding_bag per table, then a
+    concatenation into the [B][sum D] send layout (every pooled vector
+    written into its destination row).  For comparison only: it is PyTorch's
+    kernel, not this library's."""
+    import torch
+    import torch.nn.functional as F
+    w, inp, dev, send, _ = _setup(name)
+    s = torch.cuda.current_stream()
+    offs = [(dev.offsets[t * w.B:(t + 1) * w.B] - dev.offsets[t * w.B]).contiguous() for t in range(w.T)]
+    idx = [dev.indices[int(inp.offsets[t * w.B]):int(inp.offsets[(t + 1) * w.B])].long() for t in range(w.T)]
+    wts = None if dev.weights is None else [dev.weights[int(inp.offsets[t * w.B]):int(inp.offsets[(t + 1) * w.B])]
+                                            for t in range(w.T)]
+
+    def step():
+        outs = [F.embedding_bag(idx[t], dev.tables[t], offs[t], mode="sum",
+                                per_sample_weights=None if wts is None else wts[t].to(dev.tables[t].dtype))
+                for t in range(w.T)]
+        torch.cat([o.float() for o in outs], dim=1, out=send)
+
+    for _ in range(warmup):
+        step()
+    ms = time_launches(step, steps, s)
+    alg = algorithmic_bytes(w, inp.lengths, inp.weights is not None)
+    row = {"operator": "torch_embedding_bag_then_concat", "workload": name, "us": round(ms * 1e3, 1),
+           "algorithmic_gbs": round(alg / ms / 1e6, 1), "pct_hbm_peak": round(100 * alg / ms / 1e6 / HBM_PEAK_GBS, 2),
+           "torch": torch.__version__,
+           "note": "per-table F.embedding_bag (storage dtype) + cat into [B][sum D] fp32; indices widened to int64 "
+                   "beforehand (not timed)"}
+    print(json.dumps(row), flush=True)
+    return row
+
+
 def run_stream_probe(reps=20):
     """Streaming ceilings: reads (synth_stream_read, 16-byte non-temporal
     loads, 8 in flight per lane; best of several grid sizes) and writes
@@ -860,6 +894,7 @@ def main():
     ap.add_argument("--backward", action="store_true", help="embedding backward fused with the gradient's arrival")
     ap.add_argument("--backward-sweep", action="store_true", help="backward kernel time per launch shape")
     ap.add_argument("--stream-probe", action="store_true", help="streaming read and write ceilings")
+    ap.add_argument("--torch-baseline", action="store_true", help="PyTorch's embedding_bag path, for comparison")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize, a.dispatches))
@@ -885,6 +920,10 @@ def main():
         return 0
     if a.stream_probe:
         run_stream_probe()
+        return 0
+    if a.torch_baseline:
+        for n in (["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
+            run_torch_baseline(n, a.steps, a.warmup)
         return 0
     if a.row_probe:
         run_row_probe()
