@@ -207,6 +207,42 @@ def run_torch_baseline(name, steps, warmup):
            "note": "per-table F.embedding_bag (storage dtype) + cat into [B][sum D] fp32; indices widened to int64 "
                    "beforehand (not timed)"}
     print(json.dumps(row), flush=True)
+    # The backward the same way: autograd of the per-table embedding_bag
+    # with sparse=True, whose table gradients hold one row per lookup (the
+    # values ebag_a2a_backward writes); only the backward call is timed.
+    for t in range(w.T):
+        dev.tables[t].requires_grad_(True)
+    grad = torch.randn((w.B, w.sum_dim), generator=torch.Generator(device="cuda").manual_seed(2305), device="cuda")
+    col = 0
+    grads = []
+    for t in range(w.T):
+        grads.append(grad[:, col:col + w.dims[t]].to(dev.tables[t].dtype).contiguous())
+        col += w.dims[t]
+    times = []
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for it in range(warmup + steps):
+        for t in range(w.T):
+            dev.tables[t].grad = None
+        outs = [F.embedding_bag(idx[t], dev.tables[t], offs[t], mode="sum", sparse=True,
+                                per_sample_weights=None if wts is None else wts[t].to(dev.tables[t].dtype))
+                for t in range(w.T)]
+        torch.cuda.synchronize()
+        ev0.record(s)
+        torch.autograd.backward(outs, grads)
+        ev1.record(s)
+        torch.cuda.synchronize()
+        if it >= warmup:
+            times.append(ev0.elapsed_time(ev1))
+    ms = sum(times) / len(times)
+    bb = backward_bytes(w, inp.lengths, inp.weights is not None)
+    brow = {"operator": "torch_embedding_bag_sparse_backward", "workload": name, "us": round(ms * 1e3, 1),
+            "algorithmic_gbs": round(bb / ms / 1e6, 1), "torch": torch.__version__,
+            "note": "autograd of per-table F.embedding_bag(sparse=True): sparse table gradients with one row per "
+                    "lookup; the backward call alone is timed"}
+    print(json.dumps(brow), flush=True)
+    for t in range(w.T):
+        dev.tables[t].requires_grad_(False)
+        dev.tables[t].grad = None
     return row
 
 
