@@ -246,6 +246,34 @@ def run_torch_baseline(name, steps, warmup):
     return row
 
 
+def run_torch_gemv_baseline(steps, warmup, R=4):
+    """PyTorch's path for GEMV + AllReduce on one GPU: torch.mv of every
+    rank's fp16 block (the vendor BLAS), then a sum of the R partial vectors
+    in fp32 -- for comparison with the fused operator's shapes."""
+    import torch
+    s = torch.cuda.current_stream()
+    out = []
+    for M, K in GEMV_SHAPES:
+        Ks = [K // R] * R
+        g = torch.Generator(device="cuda").manual_seed(2305 + M)
+        A = [torch.randn((M, k), generator=g, device="cuda").half() for k in Ks]
+        x = [torch.randn((k,), generator=g, device="cuda").half() for k in Ks]
+
+        def step():
+            torch.stack([torch.mv(A[r], x[r]).float() for r in range(R)]).sum(0)
+
+        for _ in range(warmup):
+            step()
+        ms = time_launches(step, steps, s)
+        nbytes = gemv_ar_bytes(R, M, K, 2)
+        row = {"operator": "torch_mv_then_sum", "ranks": R, "M": M, "K": K, "us": round(ms * 1e3, 1),
+               "algorithmic_gbs": round(nbytes / ms / 1e6, 1), "torch": torch.__version__}
+        print(json.dumps(row), flush=True)
+        out.append(row)
+        del A, x
+    return out
+
+
 def run_stream_probe(reps=20):
     """Streaming ceilings: reads (synth_stream_read, 16-byte non-temporal
     loads, 8 in flight per lane; best of several grid sizes) and writes
@@ -960,6 +988,8 @@ def main():
     if a.torch_baseline:
         for n in (["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
             run_torch_baseline(n, a.steps, a.warmup)
+        if a.all:
+            run_torch_gemv_baseline(a.steps, a.warmup)
         return 0
     if a.row_probe:
         run_row_probe()
