@@ -229,7 +229,12 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
  * src into dst (same layout, [B * sum(D)] fp32) in slice order and, once a
  * slice is stored (device-scope stores), adds 1 to its flag in flags (the
  * layout of the forward's flags for this plan).  Used to feed
- * ebag_a2a_backward from a second stream.
+ * ebag_a2a_backward from a second stream: on one GPU it plays the gradient
+ * All-to-All whose arrival the backward overlaps (Sec. IV-D), the receiving
+ * side of the flags of Sec. III-A.  Grid: the plan's consumer_wgs
+ * single-wavefront workgroups.  Errors: EBAG_EINVAL for a null plan, buffer
+ * or flags, misaligned buffers or a bad B / R split, checked before anything
+ * is enqueued.
  */
 int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags, int64_t B, int32_t R,
                      hipStream_t stream);
@@ -249,8 +254,9 @@ int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_fla
  */
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]);
 
-/* Zero the slice counters, the persistent-grid ticket and the status word
- * (after a timeout or an aborted sequence).  Synchronous. */
+/* Zero the slice counters, the persistent-grid ticket, the delivery's piece
+ * counters and the status word (after a timeout or an aborted sequence).
+ * Synchronous. */
 int ebag_a2a_reset(ebag_a2a_t h);
 
 /*
