@@ -318,17 +318,6 @@ __device__ __forceinline__ void reduce_store(float* acc, int vs, int lane, float
   }
 }
 
-// Values that are the same in every lane but that the compiler cannot prove
-// so (loaded with vector loads from memory the kernel also writes): move them
-// to scalar registers explicitly.
-__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
-  return ((uint64_t)hi << 32) | lo;
-}
-
-__device__ __forceinline__ int32_t uniform32(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
-
 // Read-only inputs read with wave-uniform addresses (table order, table
 // constants and pointers, CSR offsets) go through the scalar data cache:
 // their latency then does not queue behind the row gathers in the vector
@@ -382,12 +371,6 @@ __device__ __forceinline__ void store_rows(const float* lds, int nb, int s4, flo
     const float4 x = l4[e];
     store16(rs, (int)((int64_t)i * stride * 4) + c4 * 16, x.x, x.y, x.z, x.w, sc1);
   }
-}
-
-__device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
-  const int32_t lo = __builtin_amdgcn_readlane((int32_t)(uint32_t)(uint64_t)x, l);
-  const int32_t hi = __builtin_amdgcn_readlane((int32_t)((uint64_t)x >> 32), l);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
 // Completion of one run (fused only).  release_mode 0: the workgroup's
