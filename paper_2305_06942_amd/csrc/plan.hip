@@ -218,24 +218,13 @@ int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32
   if (!tables) return fail(EBAG_EINVAL, "null table pointer array");
   if (!offsets || !send_buf || !flags) return fail(EBAG_EINVAL, "null offsets, send_buf or flags");
   if (!indices) return fail(EBAG_EINVAL, "null indices");
-  if (B <= 0 || R <= 0) return fail(EBAG_EINVAL, "B and R must be positive (B=%lld R=%d)", (long long)B, R);
-  if (B > h->max_batch) return fail(EBAG_EINVAL, "B=%lld exceeds max_batch=%lld", (long long)B, (long long)h->max_batch);
-  if (R > h->max_ranks) return fail(EBAG_EINVAL, "R=%d exceeds max_ranks=%d", R, h->max_ranks);
-  if (B % R != 0) return fail(EBAG_EINVAL, "B=%lld is not a multiple of R=%d", (long long)B, R);
-  const int64_t S = B / R;
-  if (S % h->C != 0) return fail(EBAG_EINVAL, "B/R=%lld is not a multiple of chunk_samples=%d", (long long)S, h->C);
+  const int rc = check_split(h, B, R, so);
+  if (rc) return rc;
   if (!aligned16(send_buf)) return fail(EBAG_EINVAL, "send_buf is not 16-byte aligned");
   for (int32_t t = 0; t < h->T; ++t) {
     if (!tables[t] && h->meta[t].rows > 0) return fail(EBAG_EINVAL, "null pointer for table %d", t);
     if (!aligned16(tables[t])) return fail(EBAG_EINVAL, "table %d is not 16-byte aligned", t);
   }
-  if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
-    return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
-  so->n_chunks = B / h->C;
-  so->per_rank = S / h->C;
-  so->self = h->opts.self_rank;
-  so->order = h->opts.chunk_order;
-  so->table_groups = h->table_groups;
   return EBAG_OK;
 }
 
@@ -244,6 +233,7 @@ int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32
 // array may be reused immediately.
 int sync_tables(ebag_a2a_plan* h, const void* const* tables, hipStream_t stream) {
   if (h->tables_valid && std::memcmp(h->host_tables.data(), tables, sizeof(void*) * h->T) == 0) return EBAG_OK;
+  h->tables_valid = false;  // stays false unless this upload completes
   std::memcpy(h->host_tables.data(), tables, sizeof(void*) * h->T);
   HIP_TRY(hipMemcpyAsync(h->d_tables, h->host_tables.data(), sizeof(void*) * h->T, hipMemcpyHostToDevice, stream),
           "upload table pointers");
@@ -525,10 +515,9 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   if (!h) return fail(EBAG_EINVAL, "null plan");
   if (!send_buf || !flags || !recv_buf) return fail(EBAG_EINVAL, "null send_buf, flags or recv_buf");
   if (!aligned16(send_buf) || !aligned16(recv_buf)) return fail(EBAG_EINVAL, "send/recv not 16-byte aligned");
-  if (B <= 0 || R <= 0 || B > h->max_batch || R > h->max_ranks || B % R || (B / R) % h->C)
-    return fail(EBAG_EINVAL, "bad B=%lld / R=%d for this plan", (long long)B, R);
-  if (h->opts.chunk_order == 1 && h->opts.self_rank >= R)
-    return fail(EBAG_EINVAL, "self_rank=%d is not a destination (R=%d)", h->opts.self_rank, R);
+  SliceOrder so;
+  const int rc = check_split(h, B, R, &so);
+  if (rc) return rc;
   if (capturing(stream))
     return fail(EBAG_EUNSUPPORTED, "consume waits for a fixed epoch; it cannot be captured into a graph");
   ConsumeArgs c;
@@ -540,10 +529,7 @@ int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags,
   c.trace_drain = h->opts.trace ? h->d_trace_drain : nullptr;
   c.chunk_floats = (int64_t)h->C * h->sum_dim;
   c.timeout_ticks = (uint64_t)((double)h->opts.consume_timeout_us * h->ticks_per_us);
-  c.so.n_chunks = B / h->C;
-  c.so.per_rank = (B / R) / h->C;
-  c.so.self = h->opts.self_rank;
-  c.so.order = h->opts.chunk_order;
+  c.so = so;  // the producer's order, table-major included
   c.epoch = expected_epoch;
   c.coherent_loads = h->opts.release_mode == 1;
   c.nontemporal = h->opts.consume_nontemporal;
