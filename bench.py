@@ -46,12 +46,9 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    its stream does not displace the producer's cached rows, with 1024-2048
 #    single-wave workgroups for the many short per-table items; dlrm streams
 #    its rows and keeps the defaults.
-PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1,
-                        "consumer_wgs": 1024},
-             "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
-                       "consumer_wgs": 2048},
-             "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
-                       "consumer_wgs": 1024}}
+PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
+             "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1},
+             "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1}}
 # Options that only steer the consumer (and, for the forward, the backward):
 # they do not change what a profiled kernel does.
 _NOT_FORWARD = {"consumer_wgs", "consume_nontemporal", "consume_timeout_us", "backward_bags_per_run",
