@@ -52,8 +52,8 @@ PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, 
 # Options that only steer the consumer (and, for the forward, the backward):
 # they do not change what a profiled kernel does.
 _NOT_FORWARD = {"consumer_wgs", "consume_nontemporal", "consume_timeout_us", "backward_bags_per_run",
-                "backward_waves_per_wg"}
-_NOT_BACKWARD = {"consumer_wgs", "consume_nontemporal", "stream_rows", "persistent_wgs_per_cu", "rows_in_flight",
+                "backward_waves_per_wg", "deliver_wgs"}
+_NOT_BACKWARD = {"consumer_wgs", "consume_nontemporal", "deliver_wgs", "stream_rows", "persistent_wgs_per_cu", "rows_in_flight",
                  "waves_per_wg", "bags_per_run", "check_indices", "release_mode"}
 
 
