@@ -215,16 +215,21 @@ class Plan:
         _need(send, 4 * int(B) * sum(self.dims), "send buffer")
         _need(flags, 4 * self.n_flags(int(B)), "flags")
 
+    def _offsets(self, B, offsets):
+        _need(offsets, 8 * (self.T * int(B) + 1), "offsets")
+        return _addr(offsets)
+
     def forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
-        _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), self._indices(indices), _addr(offsets),
-                                          _addr(weights), int(B), int(R), _addr(send), _addr(flags), _stream(stream)))
+        _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), self._indices(indices),
+                                          self._offsets(B, offsets), _addr(weights), int(B), int(R), _addr(send),
+                                          _addr(flags), _stream(stream)))
 
     def unfused_forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
-        _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), self._indices(indices), _addr(offsets),
-                                                  _addr(weights), int(B), int(R), _addr(send), _addr(flags),
-                                                  _stream(stream)))
+        _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), self._indices(indices),
+                                                  self._offsets(B, offsets), _addr(weights), int(B), int(R),
+                                                  _addr(send), _addr(flags), _stream(stream)))
 
     def consume(self, send, flags, recv, B, R, expected_epoch, stream=None):
         self._fwd_sizes(B, send, flags)
@@ -235,7 +240,7 @@ class Plan:
     def backward(self, grad, offsets, weights, B, R, values, grad_flags=None, expected_epoch=0, stream=None):
         self._fwd_sizes(B, grad, grad_flags)
         _check(self._lib.ebag_a2a_backward(self._h, _addr(grad), _addr(grad_flags), int(expected_epoch) & 0xFFFFFFFF,
-                                           _addr(offsets), _addr(weights), int(B), int(R), _addr(values),
+                                           self._offsets(B, offsets), _addr(weights), int(B), int(R), _addr(values),
                                            _stream(stream)))
 
     def deliver(self, src, dst, flags, B, R, stream=None):

@@ -131,3 +131,41 @@ def test_gemv_null_plan_rejected(lib):
     o = ebag.gemv_default_opts()
     assert (o.tile_rows, o.waves_per_wg, o.comm_aware, o.debug_suppress_flag, o.reduce_mode) == (0, 2, 1, -1, 0)
     lib.gemv_ar_destroy(None)
+
+
+class _NoCalls:
+    """Stands in for the loaded library: any entry point called fails the test."""
+
+    def __getattr__(self, name):
+        def call(*a):
+            raise AssertionError(f"{name} reached the C ABI with an undersized buffer")
+        return call
+
+
+def _sizing_plan(T=2, dims=(64, 32), C=8):
+    import paper_2305_06942_amd as ebag
+    p = object.__new__(ebag.Plan)
+    p.T, p.dims, p.C = T, list(dims), C
+    p.opts = ebag.default_opts()
+    p._h, p._lib, p._tab_cache, p._empty_idx = None, _NoCalls(), None, None
+    return p
+
+
+@pytest.mark.parametrize("short", ["send", "flags", "offsets"])
+def test_binding_rejects_undersized_buffers(lib, short):
+    """The binding checks tensor sizes before any call: send [B][sum D] fp32,
+    flags one uint32 per slice, offsets T*B+1 int64."""
+    import torch
+    p = _sizing_plan()
+    B, R = 32, 2
+    send = torch.zeros(B * sum(p.dims) - (4 if short == "send" else 0))
+    flags = torch.zeros(B // p.C - (1 if short == "flags" else 0), dtype=torch.int32)
+    offsets = torch.zeros(p.T * B + 1 - (1 if short == "offsets" else 0), dtype=torch.int64)
+    tables = [torch.zeros(16, d) for d in p.dims]
+    idx = torch.zeros(4, dtype=torch.int32)
+    for call in (p.forward, p.unfused_forward):
+        with pytest.raises(ValueError, match=short):
+            call(tables, idx, offsets, None, B, R, send, flags, stream=0)
+    if short != "send":
+        with pytest.raises(ValueError, match=short):
+            p.backward(send, offsets, None, B, R, torch.zeros(8), grad_flags=flags, stream=0)
