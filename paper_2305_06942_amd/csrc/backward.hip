@@ -114,8 +114,11 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   __syncthreads();
   // The run's output is one contiguous block of (lookups of its bags) x dim
   // floats; the whole workgroup streams it out.  Each thread walks float4
-  // elements tid, tid + blockDim, ... keeping its (row, vector, bag) position
-  // incrementally: no division inside the loop.
+  // elements tid, tid + blockDim, ... keeping its (row, vector) position
+  // incrementally (no division inside the loop) and the end of its current
+  // bag in a register (LDS is read only when a bag boundary is crossed).
+  // Four elements at a time: their LDS rows and weights are all requested
+  // before the first store.
   const int64_t rows = s_off[nb];
   const int64_t n = rows * V;
   f4v* out = reinterpret_cast<f4v*>(a.values + sld(a.value_base, t) + (lo0 - sld(a.offsets, (int64_t)t * a.B)) * dim);
@@ -124,17 +127,34 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   int64_t k = tid / V;
   int c = tid - (tid / V) * V;
   int bag = 0;
+  int64_t bag_end = s_off[1];  // nb >= 1
   const float* wts = a.weights ? a.weights + lo0 : nullptr;
-  for (int64_t e = tid; e < n; e += step) {
-    while (bag < nb - 1 && k >= s_off[bag + 1]) ++bag;
-    f4v x = s_lds[bag * V + c];
-    if (wts) x = wts[k] * x;
-    __builtin_nontemporal_store(x, out + e);
-    k += dk;
-    c += dc;
-    if (c >= V) {
-      c -= V;
-      ++k;
+  constexpr int UB = 4;
+  for (int64_t e0 = tid; e0 < n; e0 += (int64_t)UB * step) {
+    f4v x[UB];
+    float wv[UB];
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const bool in = e0 + (int64_t)u * step < n;
+      // k < rows = s_off[nb] for every element in range, so the walk stops
+      // at a bag below nb.
+      if (in)
+        while (k >= bag_end) bag_end = s_off[++bag + 1];
+      x[u] = s_lds[bag * V + c];
+      wv[u] = wts && in ? wts[k] : 1.f;
+      k += dk;
+      c += dc;
+      if (c >= V) {
+        c -= V;
+        ++k;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      if (e0 + (int64_t)u * step < n) {
+        const f4v y = wts ? wv[u] * x[u] : x[u];
+        __builtin_nontemporal_store(y, out + e0 + (int64_t)u * step);
+      }
     }
   }
 }
