@@ -46,9 +46,11 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    its stream does not displace the producer's cached rows, with 1024-2048
 #    single-wave workgroups for the many short per-table items; dlrm streams
 #    its rows and keeps the defaults.
-PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1},
+PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1,
+                        "backward_bags_per_run": 3},
              "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1},
-             "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1}}
+             "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
+                       "backward_bags_per_run": 8}}
 # Options that only steer the consumer (and, for the forward, the backward):
 # they do not change what a profiled kernel does.
 _NOT_FORWARD = {"consumer_wgs", "consume_nontemporal", "consume_timeout_us", "backward_bags_per_run",
@@ -771,19 +773,21 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
 
 def run_backward_sweep(name, steps, warmup):
     """Backward kernel time over its launch shape: bags and waves per
-    workgroup (the gradient complete; one JSON line per shape)."""
+    workgroup (the gradient complete; one JSON line per shape), in the
+    workload's own run order and slices (its PLAN_OPTS)."""
     import torch
     import paper_2305_06942_amd as ebag
     w, inp, dev, _, _ = _setup(name)
+    opts = {k: v for k, v in PLAN_OPTS.get(name, {}).items() if not k.startswith("backward_")}
     n_vals = int(sum((inp.offsets[(t + 1) * w.B] - inp.offsets[t * w.B]) * w.dims[t] for t in range(w.T)))
     values = torch.empty((n_vals,), device="cuda")
     grad = torch.randn((w.B, w.sum_dim), generator=torch.Generator(device="cuda").manual_seed(2305), device="cuda")
     nbytes = backward_bytes(w, inp.lengths, inp.weights is not None)
     s = torch.cuda.current_stream()
     for waves in (4, 8, 16):
-        for bags in (1, 2, 3, 4, 8, 16):
+        for bags in (1, 2, 3, 4, 6, 8, 16):
             plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, backward_waves_per_wg=waves,
-                             backward_bags_per_run=bags)
+                             backward_bags_per_run=bags, **opts)
             f = lambda: plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
             for _ in range(warmup):
                 f()
@@ -992,7 +996,7 @@ def main():
         run_row_probe()
         return 0
     if a.backward_sweep:
-        for n in (["dlrm", "large", "mixed"] if a.all else [a.workload]):
+        for n in (["dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]):
             run_backward_sweep(n, a.steps, a.warmup)
         return 0
     if a.backward:

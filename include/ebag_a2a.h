@@ -111,9 +111,9 @@ typedef struct ebag_a2a_opts {
   int32_t slice_granule;       /* 0 (default): a flag per (destination, C samples) for all T tables;
                                   1: a flag per (destination, C samples, table) -- the paper's per-table
                                   slice (Sec. III-A); see "Slices" above */
-  int32_t backward_bags_per_run;  /* ebag_a2a_backward: bags per workgroup (default 2; capped so that the
+  int32_t backward_bags_per_run;  /* ebag_a2a_backward: bags per workgroup (default 4; capped so that the
                                      bags' gradient rows fit in 64 KiB of LDS) */
-  int32_t backward_waves_per_wg;  /* ebag_a2a_backward: wavefronts per workgroup, 1..16 (default 8) */
+  int32_t backward_waves_per_wg;  /* ebag_a2a_backward: wavefronts per workgroup, 1..16 (default 16) */
   int32_t table_major;         /* 0 (default): runs slice by slice, tables fastest inside a slice; 1: table
                                   by table, slices in order inside each table, and (when T is a multiple
                                   of the XCD count) each XCD working through its own tables one at a time,

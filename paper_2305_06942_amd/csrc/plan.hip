@@ -336,8 +336,8 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
   o->consumer_wgs = 512;
   o->stream_rows = 1;
   o->consume_timeout_us = 5000000;
-  o->backward_bags_per_run = 2;
-  o->backward_waves_per_wg = 8;
+  o->backward_bags_per_run = 4;
+  o->backward_waves_per_wg = 16;
   o->deliver_wgs = 2048;
   return EBAG_OK;
 }

@@ -41,7 +41,7 @@ def test_default_opts(lib):
     import paper_2305_06942_amd as ebag
     o = ebag.default_opts()
     assert (o.waves_per_wg, o.rows_in_flight, o.debug_suppress_flag) == (4, 8, -1)
-    assert (o.backward_bags_per_run, o.backward_waves_per_wg) == (2, 8)
+    assert (o.backward_bags_per_run, o.backward_waves_per_wg) == (4, 16)
     assert (o.consumer_wgs, o.deliver_wgs) == (512, 2048)
 
 
