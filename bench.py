@@ -123,6 +123,19 @@ def time_launches(fn, steps, stream):
     return start.elapsed_time(end) / steps  # ms per launch sequence
 
 
+def time_each(fn, steps, stream):
+    """Per-launch times (ms): an event pair on `stream` around every launch."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
 def hbm_probe(nbytes=4 << 30, reps=10):
     """Achievable copy bandwidth (read + write bytes / time) with a 16-byte
     vector copy kernel."""
@@ -434,6 +447,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
     for _ in range(warmup):
         unfused()
     unfused_ms = time_launches(unfused, steps, stream)
+    # the same launches one at a time, for the median and the fastest
+    each = {} if profile else {"fused": time_each(fused, steps, stream), "unfused": time_each(unfused, steps, stream)}
     log(f"[{name}] fused {fused_ms * 1e3:.1f} us  unfused {unfused_ms * 1e3:.1f} us")
     assert np.all(flags.cpu().numpy().view(np.uint32) == epoch[0]), "flags do not match the number of forwards"
 
@@ -461,6 +476,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
         "fused_us": round(fused_ms * 1e3, 2),
         "unfused_us": round(unfused_ms * 1e3, 2),
         "fused_speedup_vs_unfused": round(unfused_ms / fused_ms, 4),
+        **{f"{k}_us_{stat}": round(f(v) * 1e3, 2) for k, v in each.items()
+           for stat, f in (("median", lambda x: float(np.median(x))), ("min", min))},
         "pct_hbm_peak": round(100 * alg / (fused_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
         "algorithmic_bytes": alg,
         "plan_options": opts,
