@@ -118,3 +118,40 @@ def test_table_major_full_size_skewed():
     check_sampled(inp, send, n_bags=400)
     del dev, send
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("major", [0, 2], ids=["slice_major", "device"])
+def test_consumer_drains_in_production_order(major):
+    """The consumer takes (slice, table) items in the producer's run order.
+    With one consumer workgroup and one flag never published, exactly the
+    items before the missing one in that order are copied, and no other.
+    (T = 5 is not a multiple of the XCD count, so table positions are the
+    tables themselves.)"""
+    import torch
+    w = synth.scaled(synth.TINY, rows=1000, B=256, T=5, R=2, C=16, name="tiny_t5")  # 16 slices
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    T, n = w.T, w.n_chunks
+    g_k, t_k = 5, 2
+    k = g_k * T + t_k
+    plan = make_plan(w, slice_granule=1, table_major=major, consumer_wgs=1, debug_suppress_flag=k,
+                     consume_timeout_us=100_000)
+    send, recv, _ = new_buffers(w)
+    flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
+    run(plan, w, dev, send, flags)
+    torch.cuda.synchronize()
+    plan.consume(send, flags, recv, w.B, w.R, 1)
+    timed_out, missing = plan.status()
+    assert (timed_out, missing) == (1, k)
+    plan.reset()
+    s, r = send.cpu().numpy(), recv.cpu().numpy()
+    off = np.cumsum([0] + list(w.dims))
+    for g in range(n):
+        for t in range(T):
+            before = (g, t) < (g_k, t_k) if major == 0 else (t, g) < (t_k, g_k)
+            bs = s[g * w.C:(g + 1) * w.C, off[t]:off[t + 1]]
+            br = r[g * w.C:(g + 1) * w.C, off[t]:off[t + 1]]
+            if before:
+                assert np.array_equal(br.view(np.uint32), bs.view(np.uint32)), f"item (slice {g}, table {t}) not drained"
+            else:
+                assert np.all(np.isnan(br)), f"item (slice {g}, table {t}) drained out of the producer's order"
