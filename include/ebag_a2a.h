@@ -134,7 +134,9 @@ typedef struct ebag_a2a_opts {
 int ebag_a2a_default_opts(ebag_a2a_opts_t* opts);
 
 /*
- * Create a plan for T tables on the current HIP device.
+ * Create a plan for T tables on the current HIP device.  Every later call on
+ * the plan must be made with that device current (EBAG_EINVAL otherwise),
+ * with buffers and a stream of that device.
  *   rows_per_table[T], dim_per_table[T]: host arrays; rows >= 0 (< 2^31), D > 0,
  *     D * elt % 16 == 0.
  *   table_dtype: storage type shared by all tables; pooled output is fp32.

@@ -85,7 +85,9 @@ int gemv_ar_default_opts(gemv_ar_opts_t* opts);
  * K[r] columns per rank (host array of R values, each > 0 with K[r] * elt a
  * multiple of 16, K[r] * elt at most 64 KiB), storage type dtype.  The plan
  * owns the reduction slots (R * M floats), the peer flags, the arrival
- * counters and a status word.  One forward may be in flight per plan.
+ * counters and a status word.  One forward may be in flight per plan.  The
+ * forwards must be called with the plan's device current (EBAG_EINVAL
+ * otherwise).
  */
 int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_dtype_t dtype,
                    const gemv_ar_opts_t* opts);

@@ -396,6 +396,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int fill_args(gemv_ar_plan* h, const void* const* A, const void* const* x, float* const* y, uint32_t* out_flags,
               GemvArgs* a) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device)
+    return fail(EBAG_EINVAL, "the plan belongs to device %d, but device %d is current", h->device, dev);
   if (!A || !x || !y) return fail(EBAG_EINVAL, "null A, x or y pointer array");
   std::memset(a, 0, sizeof *a);
   for (int r = 0; r < h->R; ++r) {

@@ -194,6 +194,9 @@ int check_opts(const ebag_a2a_opts_t& o) {
 // B / R checks shared by every entry point that walks slices; fills the
 // slice order.
 int check_split(const ebag_a2a_plan* h, int64_t B, int32_t R, SliceOrder* so) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device)
+    return fail(EBAG_EINVAL, "the plan belongs to device %d, but device %d is current", h->device, dev);
   if (B <= 0 || R <= 0) return fail(EBAG_EINVAL, "B and R must be positive (B=%lld R=%d)", (long long)B, R);
   if (B > h->max_batch) return fail(EBAG_EINVAL, "B=%lld exceeds max_batch=%lld", (long long)B, (long long)h->max_batch);
   if (R > h->max_ranks) return fail(EBAG_EINVAL, "R=%d exceeds max_ranks=%d", R, h->max_ranks);
