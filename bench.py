@@ -986,7 +986,7 @@ def main():
         print(json.dumps(traffic(a.traffic[0], a.traffic[1], a.workload, kernel=kernel), indent=1))
         return 0
     if a.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
+        print(f"bench.py: the benchmark runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
               "are logical slices of one GPU's send buffer)", file=sys.stderr)
         return 2
     import torch

@@ -79,7 +79,7 @@ typedef enum { EBAG_F32 = 0, EBAG_F16 = 1, EBAG_BF16 = 2 } ebag_dtype_t;
 enum {
   EBAG_OK = 0,
   EBAG_EINVAL = -1,       /* bad argument (null pointer, size, split, alignment) */
-  EBAG_EUNSUPPORTED = -2, /* valid but not supported by this build */
+  EBAG_EUNSUPPORTED = -2, /* valid, but outside what the library supports */
   EBAG_EHIP = -3,         /* a HIP runtime call failed */
   EBAG_ETIMEOUT = -4,     /* reported by ebag_a2a_status() */
   EBAG_ENOMEM = -5,       /* device or host allocation failed */
