@@ -31,8 +31,11 @@ KERNEL_SOURCES = {
     "fused_pool_kernel": ["paper_2305_06942_amd/csrc/pool.hip", "paper_2305_06942_amd/csrc/common.h"],
     "backward_kernel": ["paper_2305_06942_amd/csrc/backward.hip", "paper_2305_06942_amd/csrc/backward.h",
                         "paper_2305_06942_amd/csrc/common.h"],
+    "gemv_ar_last_arriver_kernel": ["paper_2305_06942_amd/csrc/gemv_ar.hip"],
 }
-TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json"}
+# GEMV + AllReduce records are keyed by the output size: workload "m<M>".
+TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traffic_backward_{}.json",
+                "gemv_ar_last_arriver_kernel": "traffic_gemv_{}.json"}
 # Launch options per workload (every other option at its default):
 #  * where rows are reused -- Zipf indices (skewed, large), or tables small
 #    enough for the Infinity Cache (mixed's 64-256 MB tables) -- rows are
@@ -826,10 +829,11 @@ def gemv_ar_bytes(R, M, K, elt):
     return M * K * elt + K * elt + 2 * R * M * 4 + R * M * 4
 
 
-def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
-    """GEMV + AllReduce (Sec. III-B) on R logical ranks: fused (one
-    cooperative launch) against bulk-synchronous (GEMV kernel, then AllReduce
-    kernel, then flags), one JSON line per shape."""
+def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True, profile=False):
+    """GEMV + AllReduce (Sec. III-B) on R logical ranks: fused (one launch;
+    the last arriver reduces) against bulk-synchronous (GEMV kernel, then
+    AllReduce kernel, then flags), one JSON line per shape.  profile: also
+    two 1 GiB copies that calibrate the byte counters."""
     import numpy as np
     import torch
     import paper_2305_06942_amd as ebag
@@ -860,8 +864,22 @@ def run_gemv_ar(steps, warmup, R=4, dtype=1, shapes=GEMV_SHAPES, with_cpu=True):
                "fused_us": round(f_ms * 1e3, 2), "unfused_us": round(u_ms * 1e3, 2),
                "fused_speedup_vs_unfused": round(u_ms / f_ms, 4), "algorithmic_bytes": nbytes,
                "roofline": {"bound": "hbm", "achieved": round(nbytes / (f_ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                            "unit": "GB/s", "frac": round(nbytes / (f_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+                            "unit": "GB/s", "frac": round(nbytes / (f_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                            "traffic": None, "kernel": "gemv_ar_last_arriver_kernel"},
                "data": "synthetic: torch.randn on the device, seeded"}
+        tr = traffic_record(f"m{M}", "gemv_ar_last_arriver_kernel")
+        if tr:
+            row["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
+        if profile:
+            # a plain copy of known size: calibrates the byte counters per dispatch
+            from synth import device as _sd
+            src = torch.ones((1 << 30) // 4, device="cuda")
+            dst = torch.empty_like(src)
+            for _ in range(2):
+                _sd.copy(dst, src, 1 << 30)
+            torch.cuda.synchronize()
+            row["calibration_copy_bytes"] = 1 << 30
+            del src, dst
         if with_cpu and M == shapes[0][0]:
             import oracle
             hA = [a.cpu().numpy() if dtype != 2 else a.view(torch.int16).cpu().numpy().view(np.uint16) for a in A]
@@ -982,8 +1000,11 @@ def main():
         print(summarize(a.summarize, a.dispatches))
         return 0
     if a.traffic:
-        kernel = "backward_kernel" if a.backward else "fused_pool_kernel"
-        print(json.dumps(traffic(a.traffic[0], a.traffic[1], a.workload, kernel=kernel), indent=1))
+        if a.gemv_ar:
+            kernel, workload = "gemv_ar_last_arriver_kernel", f"m{a.gemv_m}"
+        else:
+            kernel, workload = ("backward_kernel" if a.backward else "fused_pool_kernel"), a.workload
+        print(json.dumps(traffic(a.traffic[0], a.traffic[1], workload, kernel=kernel), indent=1))
         return 0
     if a.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
@@ -1025,7 +1046,7 @@ def main():
         if not shapes:
             print(f"bench.py: no GEMV shape with M={a.gemv_m}", file=sys.stderr)
             return 2
-        run_gemv_ar(a.steps, a.warmup, shapes=shapes, with_cpu=not (a.no_cpu_baseline or a.profile))
+        run_gemv_ar(a.steps, a.warmup, shapes=shapes, with_cpu=not (a.no_cpu_baseline or a.profile), profile=a.profile)
         return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:
