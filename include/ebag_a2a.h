@@ -90,7 +90,9 @@ enum {
  * fill with ebag_a2a_default_opts() and change fields. */
 typedef struct ebag_a2a_opts {
   int32_t waves_per_wg;        /* wavefronts (64 lanes) per pooling workgroup, 1..16 (default 4) */
-  int32_t bags_per_run;        /* bags a workgroup pools before one slice-counter update (default 16) */
+  int32_t bags_per_run;        /* bags a workgroup pools before one slice-counter update (default 16;
+                                  capped so that the run's pooled rows, bags x max D floats, fit a 16 KiB
+                                  LDS tile, and at chunk_samples) */
   int32_t rows_in_flight;      /* 16-byte row loads each wave keeps in flight: 4, 8 or 16 (default 8) */
   int32_t persistent_wgs_per_cu; /* 0: one workgroup per run; >0: persistent grid of that many WGs per CU
                                     (-1: as many as fit), whose workgroups claim runs in production order
@@ -104,7 +106,8 @@ typedef struct ebag_a2a_opts {
   int32_t consumer_wgs;        /* single-wave workgroups of the consumer kernel (default 512) */
   int32_t stream_rows;         /* 1 (default): table rows are read with non-temporal loads (no reuse expected);
                                   0: cached loads (skewed index distributions with hot rows) */
-  int64_t consume_timeout_us;  /* consumer gives up after this long (default 5,000,000 us) */
+  int64_t consume_timeout_us;  /* the consumer, and the backward waiting on gradient flags, give up after
+                                  this long and report it through ebag_a2a_status (default 5,000,000 us) */
   int32_t pooling_mode;        /* 0 (default): sum (weighted sum when weights are given); 1: mean -- the
                                   bag's sum divided by its length L, zeros for an empty bag; takes no weights
                                   (the sum / mean modes of the original pooling kernel, Sec. III-A) */
