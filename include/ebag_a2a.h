@@ -172,6 +172,44 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
                      hipStream_t stream);
 
 /*
+ * Fused forward without a plan, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same operation, result and flag contract as
+ * ebag_a2a_forward on a plan created with the same tables, chunk_samples and
+ * opts; the table shapes (as for ebag_a2a_create) come with every call.
+ *
+ * The device memory a plan would own -- table descriptors and pointers,
+ * slice counters, status word, run ticket -- is instead one statically
+ * allocated device array of EBAG_NOALLOC_SCRATCH_BYTES per GPU, which every
+ * GPU the library runs on holds until the process ends.  Each call first
+ * enqueues a small kernel (one per 64 tables) that writes the descriptors
+ * into that array and clears the counters, ticket and status word, then the
+ * pooling kernel; it calls no hipMalloc, hipFree or other allocating routine.
+ *   num_tables: 1 .. EBAG_NOALLOC_MAX_TABLES.
+ *   opts: NULL for the defaults; trace = 1 and check_indices = 1 are refused
+ *     with EBAG_EUNSUPPORTED (their results are read through a plan);
+ *     consumer, backward and delivery options are ignored.
+ *   B / chunk_samples flags (times num_tables with slice_granule = 1) must
+ *     not exceed EBAG_NOALLOC_MAX_FLAGS (EBAG_EINVAL otherwise).
+ *   Other arguments as for ebag_a2a_create and ebag_a2a_forward; every check
+ *   is made before anything is enqueued.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: two calls that overlap on one GPU (on different streams, or from
+ * different host threads without ordering) race on it and corrupt each
+ * other's slice counters.  Order them on one stream.  The first call on a
+ * device looks up the array's device address (hipGetSymbolAddress) with that
+ * device current.
+ */
+#define EBAG_NOALLOC_MAX_TABLES 1024
+#define EBAG_NOALLOC_MAX_FLAGS 65536
+#define EBAG_NOALLOC_SCRATCH_BYTES (320 * 1024)
+int ebag_a2a_forward_noalloc(int32_t num_tables, const int64_t* rows_per_table, const int32_t* dim_per_table,
+                             ebag_dtype_t table_dtype, int32_t chunk_samples, const ebag_a2a_opts_t* opts,
+                             const void* const* tables, const int32_t* indices, const int64_t* offsets,
+                             const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
+                             hipStream_t stream);
+
+/*
  * Bulk-synchronous baseline with the same contract and result: a pooling
  * kernel writes per-table outputs [T][B][D_t] to plan scratch, then a
  * repack kernel copies them into the send layout and releases each slice's

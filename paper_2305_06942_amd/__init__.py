@@ -7,4 +7,4 @@ only: every step of the operation runs in the HIP library
 library is missing, :func:`load` raises.
 """
 from .abi import (EBAG_BF16, EBAG_F16, EBAG_F32, EbagError, GemvAR, Plan, default_opts,  # noqa: F401
-                  gemv_default_opts, last_error, load, queue_stream, queue_stream_destroy, symbols)
+                  forward_noalloc, gemv_default_opts, last_error, load, queue_stream, queue_stream_destroy, symbols)

@@ -70,6 +70,8 @@ _SIGS = {
                         ctypes.c_int),
     "ebag_a2a_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_unfused_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
+    "ebag_a2a_forward_noalloc": ([ctypes.c_int32, _P, _P, ctypes.c_int, ctypes.c_int32, _P, _P, _P, _P, _P,
+                                  ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_consume": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, _P], ctypes.c_int),
     "ebag_a2a_backward": ([_P, _P, _P, ctypes.c_uint32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P], ctypes.c_int),
     "ebag_a2a_deliver": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P], ctypes.c_int),
@@ -165,6 +167,37 @@ def default_opts() -> Opts:
     o = Opts()
     _check(load().ebag_a2a_default_opts(ctypes.byref(o)))
     return o
+
+
+NOALLOC_MAX_TABLES, NOALLOC_MAX_FLAGS = 1024, 65536
+
+
+def forward_noalloc(rows, dims, dtype, chunk_samples, tables, indices, offsets, weights, B, R, send, flags,
+                    stream=None, **opts):
+    """Plan-free fused forward (``ebag_a2a_forward_noalloc``): the same result
+    as ``Plan(rows, dims, dtype, chunk_samples, ..., **opts).forward(...)``,
+    with the plan's device memory in the library's static per-GPU array."""
+    lib = load()
+    o = default_opts()
+    for k, v in opts.items():
+        if not hasattr(o, k):
+            raise TypeError(f"unknown option {k}")
+        setattr(o, k, int(v))
+    T = len(rows)
+    if len(dims) != T or len(tables) != T:
+        raise ValueError("rows, dims and tables must have one entry per table")
+    n_flags = (int(B) // int(chunk_samples)) * (T if o.slice_granule == 1 else 1)
+    _need(send, 4 * int(B) * sum(int(d) for d in dims), "send buffer")
+    _need(flags, 4 * n_flags, "flags")
+    _need(offsets, 8 * (T * int(B) + 1), "offsets")
+    if hasattr(indices, "numel") and indices.numel() == 0:
+        raise ValueError("indices must have a device address: pass a one-element buffer when every bag is empty")
+    rows_a = (ctypes.c_int64 * T)(*[int(r) for r in rows])
+    dims_a = (ctypes.c_int32 * T)(*[int(d) for d in dims])
+    tabs = (ctypes.c_void_p * T)(*[_addr(t) for t in tables])
+    _check(lib.ebag_a2a_forward_noalloc(T, rows_a, dims_a, int(dtype), int(chunk_samples), ctypes.byref(o), tabs,
+                                        _addr(indices), _addr(offsets), _addr(weights), int(B), int(R), _addr(send),
+                                        _addr(flags), _stream(stream)))
 
 
 class Plan:

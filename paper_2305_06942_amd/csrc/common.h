@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "ebag_a2a.h"
+
 namespace ebag {
 
 // Per-table constants, resident in device memory for the plan's lifetime.
@@ -94,8 +96,40 @@ struct PoolArgs {
   int32_t per_table;          // 1: one flag / counter per (slice, table), index g * T + t
 };
 
-// Status word layout (int32[4]).
+// Host-side description of the plan behind a pooling launch: a plan from
+// ebag_a2a_create, or one assembled per call by the plan-free forward.
+struct PoolSetup {
+  const ebag_a2a_opts_t* o;
+  const TabMeta* meta;          // [T], host copy
+  int32_t T;
+  int32_t C;
+  int32_t sum_dim;
+  int32_t dtype;
+  int32_t num_cus;
+  int32_t table_groups;         // SliceOrder::table_groups under these options
+  const void* const* d_tables;  // device arrays the kernels read and write
+  const TabMeta* d_meta;
+  const int32_t* d_tperm;
+  uint32_t* d_counters;
+  int32_t* d_status;
+  uint64_t* d_trace_release;    // nullptr: no trace
+  uint32_t* d_ticket;
+};
+
+// Host helpers shared by the plan and the plan-free forward (plan.hip).
+constexpr int kMaxXcd = 64;
+int check_opts(const ebag_a2a_opts_t& o);
+int xcd_count(int num_cus);
+int32_t table_groups_for(const ebag_a2a_opts_t& o, int32_t T, int n_xcd);
+void table_order(const int64_t* row_bytes, int32_t T, int n_xcd, int32_t* perm, int32_t* work, int64_t* load);
+bool needs_safe(const PoolSetup& s);
+void fill_pool_args(const PoolSetup& s, const int32_t* indices, const int64_t* offsets, const float* weights,
+                    int64_t B, const SliceOrder& so, float* out, uint32_t* flags, PoolArgs* a);
+int pool_grid(const PoolSetup& s, int64_t nruns, bool fused, bool weighted, int block, int out_floats);
+
+// Status word layout (int32[4]) and its initial value.
 enum { ST_TIMED_OUT = 0, ST_FIRST_MISSING = 1, ST_OVERSHOOT = 2, ST_FIRST_BAD_BAG = 3 };
+constexpr int32_t kStatusInit[4] = {0, 0x7fffffff, 0, 0x7fffffff};
 
 // Error reporting shared by every entry point (thread-local message).
 int fail(int code, const char* fmt, ...);

@@ -50,6 +50,14 @@ int hip_fail(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+int log2_exact(int v) {
+  for (int s = 0; s <= 6; ++s)
+    if ((1 << s) == v) return s;
+  return -1;
+}
+
+}  // namespace
+
 // Table order inside a slice.  The dispatcher hands workgroups to the XCDs
 // round-robin (workgroup i to XCD i mod n_xcd), and runs are numbered with
 // the table position fastest, so when T is a multiple of n_xcd the runs at
@@ -58,37 +66,43 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // bytes (row width; bag lengths are unknown here): widest first, each to the
 // least-loaded XCD with room.  Tables of equal width keep t mod n_xcd, so an
 // XCD's L2 sees the hot rows of only its own tables.  Any order is correct;
-// this only balances work.
-std::vector<int32_t> table_order(const std::vector<int64_t>& row_bytes, int n_xcd) {
-  const int T = (int)row_bytes.size();
-  std::vector<int32_t> perm(T);
-  for (int t = 0; t < T; ++t) perm[t] = t;
-  if (n_xcd <= 1 || T % n_xcd != 0) return perm;
-  std::vector<int32_t> by_width(perm);
-  std::stable_sort(by_width.begin(), by_width.end(),
-                   [&](int32_t x, int32_t y) { return row_bytes[x] > row_bytes[y]; });
+// this only balances work.  Writes perm[T]; work[T] and load[n_xcd] are
+// caller-provided workspace (nothing is allocated).
+void ebag::table_order(const int64_t* row_bytes, int32_t T, int n_xcd, int32_t* perm, int32_t* work,
+                       int64_t* load) {
+  for (int32_t t = 0; t < T; ++t) perm[t] = t;
+  if (n_xcd <= 1 || n_xcd > kMaxXcd || T % n_xcd != 0) return;
+  // perm holds the tables widest first (ties in table order) until the end.
+  std::sort(perm, perm + T, [&](int32_t x, int32_t y) {
+    return row_bytes[x] != row_bytes[y] ? row_bytes[x] > row_bytes[y] : x < y;
+  });
   const int cap = T / n_xcd;
-  std::vector<int64_t> load(n_xcd, 0);
-  std::vector<std::vector<int32_t>> bins(n_xcd);
-  for (int32_t t : by_width) {
+  int count[kMaxXcd];
+  for (int x = 0; x < n_xcd; ++x) {
+    count[x] = 0;
+    load[x] = 0;
+  }
+  int32_t* bins = work;  // bin x: bins[x * cap .. x * cap + count[x])
+  for (int32_t i = 0; i < T; ++i) {
+    const int32_t t = perm[i];
     int best = -1;
     for (int x = 0; x < n_xcd; ++x)
-      if ((int)bins[x].size() < cap && (best < 0 || load[x] < load[best])) best = x;
-    bins[best].push_back(t);
+      if (count[x] < cap && (best < 0 || load[x] < load[best])) best = x;
+    bins[best * cap + count[best]++] = t;
     load[best] += row_bytes[t];
   }
   // Refine: swap a wider table of the most loaded XCD with a narrower one of
   // the least loaded while that narrows their gap (each swap strictly lowers
   // the sum of squared loads, so this ends).
   for (int it = 0; it < 2 * T; ++it) {
-    const int hi = (int)(std::max_element(load.begin(), load.end()) - load.begin());
-    const int lo = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+    const int hi = (int)(std::max_element(load, load + n_xcd) - load);
+    const int lo = (int)(std::min_element(load, load + n_xcd) - load);
     const int64_t gap = load[hi] - load[lo];
     int bi = -1, bj = -1;
     int64_t bd = 0;
     for (int i = 0; i < cap; ++i)
       for (int j = 0; j < cap; ++j) {
-        const int64_t d = row_bytes[bins[hi][i]] - row_bytes[bins[lo][j]];
+        const int64_t d = row_bytes[bins[hi * cap + i]] - row_bytes[bins[lo * cap + j]];
         if (d > 0 && d < gap && (bi < 0 || std::llabs(gap - 2 * d) < std::llabs(gap - 2 * bd))) {
           bi = i;
           bj = j;
@@ -96,24 +110,25 @@ std::vector<int32_t> table_order(const std::vector<int64_t>& row_bytes, int n_xc
         }
       }
     if (bi < 0) break;
-    std::swap(bins[hi][bi], bins[lo][bj]);
+    std::swap(bins[hi * cap + bi], bins[lo * cap + bj]);
     load[hi] -= bd;
     load[lo] += bd;
   }
   for (int x = 0; x < n_xcd; ++x) {
-    std::sort(bins[x].begin(), bins[x].end());
-    for (int k = 0; k < cap; ++k) perm[x + n_xcd * k] = bins[x][k];
+    std::sort(bins + x * cap, bins + (x + 1) * cap);
+    for (int k = 0; k < cap; ++k) perm[x + n_xcd * k] = bins[x * cap + k];
   }
-  return perm;
 }
 
-int log2_exact(int v) {
-  for (int s = 0; s <= 6; ++s)
-    if ((1 << s) == v) return s;
-  return -1;
-}
+// MI355X: 8 XCDs of 32 CUs.
+int ebag::xcd_count(int num_cus) { return (num_cus % 32 == 0 && num_cus >= 64) ? num_cus / 32 : 1; }
 
-}  // namespace
+// Table-major runs: 1 -> one table group per XCD when the tables divide
+// evenly (each XCD pools its own tables); 2 -> one table at a time for the
+// whole device.
+int32_t ebag::table_groups_for(const ebag_a2a_opts_t& o, int32_t T, int n_xcd) {
+  return o.table_major == 2 ? 1 : o.table_major == 1 ? (T % n_xcd == 0 ? n_xcd : 1) : 0;
+}
 
 struct ebag_a2a_plan {
   int device = 0;
@@ -149,8 +164,6 @@ struct ebag_a2a_plan {
 
 namespace {
 
-const int32_t kStatusInit[4] = {0, INT_MAX, 0, INT_MAX};
-
 void free_plan(ebag_a2a_plan* h) {
   if (!h) return;
   (void)hipFree(h->d_meta);
@@ -167,7 +180,9 @@ void free_plan(ebag_a2a_plan* h) {
   delete h;
 }
 
-int check_opts(const ebag_a2a_opts_t& o) {
+}  // namespace
+
+int ebag::check_opts(const ebag_a2a_opts_t& o) {
   if (o.waves_per_wg < 1 || o.waves_per_wg > 16) return fail(EBAG_EINVAL, "waves_per_wg must be in [1, 16]");
   if (o.bags_per_run < 1) return fail(EBAG_EINVAL, "bags_per_run must be >= 1");
   if (o.rows_in_flight != 4 && o.rows_in_flight != 8 && o.rows_in_flight != 16)
@@ -190,6 +205,8 @@ int check_opts(const ebag_a2a_opts_t& o) {
   if (o.deliver_wgs < 1) return fail(EBAG_EINVAL, "deliver_wgs must be >= 1");
   return EBAG_OK;
 }
+
+namespace {
 
 // B / R checks shared by every entry point that walks slices; fills the
 // slice order.
@@ -246,69 +263,96 @@ int sync_tables(ebag_a2a_plan* h, const void* const* tables, hipStream_t stream)
   return EBAG_OK;
 }
 
-void fill_pool_args(const ebag_a2a_plan* h, const int32_t* indices, const int64_t* offsets, const float* weights,
-                    int64_t B, const SliceOrder& so, float* out, uint32_t* flags, PoolArgs* a) {
+}  // namespace
+
+void ebag::fill_pool_args(const PoolSetup& s, const int32_t* indices, const int64_t* offsets, const float* weights,
+                          int64_t B, const SliceOrder& so, float* out, uint32_t* flags, PoolArgs* a) {
   std::memset(a, 0, sizeof *a);
-  int32_t K = h->opts.bags_per_run < h->C ? h->opts.bags_per_run : h->C;
+  const ebag_a2a_opts_t& o = *s.o;
+  int32_t K = o.bags_per_run < s.C ? o.bags_per_run : s.C;
   // The fast kernels keep a run's pooled rows in LDS (K x max dim floats):
   // cap that buffer at 16 KiB.
   int32_t max_dim = 0;
-  for (const TabMeta& m : h->meta) max_dim = m.dim > max_dim ? m.dim : max_dim;
+  for (int32_t t = 0; t < s.T; ++t) max_dim = s.meta[t].dim > max_dim ? s.meta[t].dim : max_dim;
   const int32_t k_cap = 16384 / (4 * max_dim) > 1 ? 16384 / (4 * max_dim) : 1;
   if (K > k_cap) K = k_cap;
-  a->tables = h->d_tables;
-  a->meta = h->d_meta;
-  a->tperm = h->d_tperm;
+  a->tables = s.d_tables;
+  a->meta = s.d_meta;
+  a->tperm = s.d_tperm;
   a->indices = indices;
   a->offsets = offsets;
   a->weights = weights;
   a->out = out;
-  a->counters = h->d_counters;
+  a->counters = s.d_counters;
   a->flags = flags;
-  a->status = h->d_status;
-  a->trace_release = h->opts.trace ? h->d_trace_release : nullptr;
-  a->ticket = h->d_ticket;
+  a->status = s.d_status;
+  a->trace_release = o.trace ? s.d_trace_release : nullptr;
+  a->ticket = s.d_ticket;
   a->B = B;
   a->K = K;
-  a->J = (h->C + K - 1) / K;
-  a->T = h->T;
-  a->C = h->C;
-  a->nruns = so.n_chunks * (int64_t)h->T * a->J;
-  a->suppress = h->opts.debug_suppress_flag;
+  a->J = (s.C + K - 1) / K;
+  a->T = s.T;
+  a->C = s.C;
+  a->nruns = so.n_chunks * (int64_t)s.T * a->J;
+  a->suppress = o.debug_suppress_flag;
   a->so = so;
-  a->sum_dim = h->sum_dim;
-  a->check = h->opts.check_indices;
-  a->release_mode = h->opts.release_mode;
-  a->waves = h->opts.waves_per_wg;
+  a->sum_dim = s.sum_dim;
+  a->check = o.check_indices;
+  a->release_mode = o.release_mode;
+  a->waves = o.waves_per_wg;
   a->out_floats = K * max_dim;
-  a->stream_rows = h->opts.stream_rows;
-  a->mean = h->opts.pooling_mode == 1;
-  a->per_table = h->opts.slice_granule == 1;
+  a->stream_rows = o.stream_rows;
+  a->mean = o.pooling_mode == 1;
+  a->per_table = o.slice_granule == 1;
 }
 
 // The fast pooling kernels handle tables below 4 GiB (32-bit buffer offsets)
 // whose rows are 2^k <= 64 sixteen-byte vectors, without index reporting;
 // anything else uses the general kernels.
-bool needs_safe(const ebag_a2a_plan* h) {
-  if (h->opts.check_indices) return true;
-  for (const TabMeta& m : h->meta)
+bool ebag::needs_safe(const PoolSetup& s) {
+  if (s.o->check_indices) return true;
+  for (int32_t t = 0; t < s.T; ++t) {
+    const TabMeta& m = s.meta[t];
     if (m.vshift < 0 || m.rows * m.row_bytes > (int64_t)0xFFFFFFFFll) return true;
+  }
   return false;
 }
 
-int pool_grid(const ebag_a2a_plan* h, int64_t nruns, bool fused, bool weighted, int block, int out_floats) {
+int ebag::pool_grid(const PoolSetup& s, int64_t nruns, bool fused, bool weighted, int block, int out_floats) {
   int64_t grid = nruns;
-  if (h->opts.persistent_wgs_per_cu != 0) {
-    int per_cu = h->opts.persistent_wgs_per_cu;
+  if (s.o->persistent_wgs_per_cu != 0) {
+    int per_cu = s.o->persistent_wgs_per_cu;
     if (per_cu < 0)
-      per_cu = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, weighted, fused, needs_safe(h), block,
-                                   out_floats);
+      per_cu = pool_max_wgs_per_cu(s.dtype, s.o->rows_in_flight, weighted, fused, needs_safe(s), block, out_floats);
     if (per_cu < 1) per_cu = 1;
-    const int64_t pg = (int64_t)per_cu * h->num_cus;
+    const int64_t pg = (int64_t)per_cu * s.num_cus;
     if (pg < grid) grid = pg;
   }
   if (grid > INT_MAX) grid = INT_MAX;
   return (int)grid;
+}
+
+namespace {
+
+// The plan as a pooling launch sees it.
+PoolSetup setup_of(const ebag_a2a_plan* h) {
+  PoolSetup s;
+  s.o = &h->opts;
+  s.meta = h->meta.data();
+  s.T = h->T;
+  s.C = h->C;
+  s.sum_dim = h->sum_dim;
+  s.dtype = h->dtype;
+  s.num_cus = h->num_cus;
+  s.table_groups = h->table_groups;
+  s.d_tables = h->d_tables;
+  s.d_meta = h->d_meta;
+  s.d_tperm = h->d_tperm;
+  s.d_counters = h->d_counters;
+  s.d_status = h->d_status;
+  s.d_trace_release = h->d_trace_release;
+  s.d_ticket = h->d_ticket;
+  return s;
 }
 
 }  // namespace
@@ -421,13 +465,11 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
     h->ticks_per_us = khz / 1000.0;
   std::vector<int64_t> widths(num_tables);
   for (int32_t t = 0; t < num_tables; ++t) widths[t] = meta[t].row_bytes;
-  // MI355X: 8 XCDs of 32 CUs.
-  const int n_xcd = (h->num_cus % 32 == 0 && h->num_cus >= 64) ? h->num_cus / 32 : 1;
-  std::vector<int32_t> tperm = table_order(widths, n_xcd);
-  // Table-major runs: 1 -> one table group per XCD when the tables divide
-  // evenly (each XCD pools its own tables); 2 -> one table at a time for the
-  // whole device.
-  h->table_groups = o.table_major == 2 ? 1 : o.table_major == 1 ? (num_tables % n_xcd == 0 ? n_xcd : 1) : 0;
+  const int n_xcd = xcd_count(h->num_cus);
+  std::vector<int32_t> tperm(num_tables), order_work(num_tables);
+  std::vector<int64_t> order_load(kMaxXcd);
+  table_order(widths.data(), num_tables, n_xcd, tperm.data(), order_work.data(), order_load.data());
+  h->table_groups = table_groups_for(o, num_tables, n_xcd);
   CREATE_TRY(hipMalloc((void**)&h->d_meta, sizeof(TabMeta) * num_tables), "alloc table meta");
   CREATE_TRY(hipMemcpy(h->d_meta, meta.data(), sizeof(TabMeta) * num_tables, hipMemcpyHostToDevice), "upload meta");
   CREATE_TRY(hipMalloc((void**)&h->d_tperm, sizeof(int32_t) * num_tables), "alloc table order");
@@ -464,11 +506,11 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   rc = sync_tables(h, tables, stream);
   if (rc) return rc;
   PoolArgs a;
-  fill_pool_args(h, indices, offsets, weights, B, so, send_buf, flags, &a);
+  fill_pool_args(setup_of(h), indices, offsets, weights, B, so, send_buf, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
   if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
-  const int grid = pool_grid(h, a.nruns, true, weights != nullptr, block, a.out_floats);
-  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(h), a, grid,
+  const int grid = pool_grid(setup_of(h), a.nruns, true, weights != nullptr, block, a.out_floats);
+  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(setup_of(h)), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
   return EBAG_OK;
@@ -483,11 +525,11 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   rc = sync_tables(h, tables, stream);
   if (rc) return rc;
   PoolArgs a;
-  fill_pool_args(h, indices, offsets, weights, B, so, h->d_scratch, flags, &a);
+  fill_pool_args(setup_of(h), indices, offsets, weights, B, so, h->d_scratch, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
   if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
-  const int grid = pool_grid(h, a.nruns, false, weights != nullptr, block, a.out_floats);
-  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(h), a, grid,
+  const int grid = pool_grid(setup_of(h), a.nruns, false, weights != nullptr, block, a.out_floats);
+  hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(setup_of(h)), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch pooling kernel");
   RepackArgs r;
@@ -698,9 +740,9 @@ int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]) {
   PoolArgs a;
   SliceOrder so;
   std::memset(&so, 0, sizeof so);
-  fill_pool_args(h, nullptr, nullptr, nullptr, 0, so, nullptr, nullptr, &a);
+  fill_pool_args(setup_of(h), nullptr, nullptr, nullptr, 0, so, nullptr, nullptr, &a);
   const int block = 64 * h->opts.waves_per_wg;
-  const int n = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, weighted != 0, true, needs_safe(h), block,
+  const int n = pool_max_wgs_per_cu(h->dtype, h->opts.rows_in_flight, weighted != 0, true, needs_safe(setup_of(h)), block,
                                     a.out_floats);
   if (n <= 0) return fail(EBAG_EHIP, "occupancy query failed");
   out[0] = n;

@@ -169,3 +169,40 @@ def test_binding_rejects_undersized_buffers(lib, short):
     if short != "send":
         with pytest.raises(ValueError, match=short):
             p.backward(send, offsets, None, B, R, torch.zeros(8), grad_flags=flags, stream=0)
+
+
+def _noalloc(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, B=256, R=2, opts=None, null_send=False):
+    r = (ctypes.c_int64 * max(T, 1))(*(list(rows) + [10] * max(T - len(rows), 0))[:max(T, 1)])
+    d = (ctypes.c_int32 * max(T, 1))(*(list(dims) + [64] * max(T - len(dims), 0))[:max(T, 1)])
+    fake = 1 << 20  # a 16-byte aligned address that is never dereferenced: every case fails on the host
+    tabs = (ctypes.c_void_p * max(T, 1))(*([fake] * max(T, 1)))
+    return lib.ebag_a2a_forward_noalloc(T, r, d, dtype, C, None if opts is None else ctypes.byref(opts), tabs,
+                                        fake, fake, None, B, R, None if null_send else fake, fake, None)
+
+
+@pytest.mark.parametrize("kw,code,msg", [
+    (dict(T=0), "EBAG_EINVAL", "num_tables"),
+    (dict(T=1025), "EBAG_EINVAL", "num_tables"),
+    (dict(dims=(64, 6)), "EBAG_EINVAL", "multiple of 16"),
+    (dict(dtype=9), "EBAG_EINVAL", "dtype"),
+    (dict(B=255), "EBAG_EINVAL", "multiple of R"),
+    (dict(B=2 * 65537 * 32, R=2), "EBAG_EINVAL", "slice counters"),
+    (dict(null_send=True), "EBAG_EINVAL", "null"),
+    (dict(opts="trace"), "EBAG_EUNSUPPORTED", "plan"),
+    (dict(opts="check_indices"), "EBAG_EUNSUPPORTED", "plan"),
+    (dict(opts="waves"), "EBAG_EINVAL", "waves_per_wg"),
+])
+def test_noalloc_rejects_before_touching_the_device(lib, kw, code, msg):
+    """Sizes beyond the static array and bad arguments fail with a clear
+    error before anything is enqueued (no GPU here)."""
+    import paper_2305_06942_amd as ebag
+    if isinstance(kw.get("opts"), str):
+        o = ebag.default_opts()
+        if kw["opts"] == "waves":
+            o.waves_per_wg = 0
+        else:
+            setattr(o, kw["opts"], 1)
+        kw = dict(kw, opts=o)
+    rc = _noalloc(lib, **kw)
+    assert rc == getattr(ebag.abi, code), (rc, ebag.last_error())
+    assert msg in ebag.last_error(), ebag.last_error()

@@ -15,7 +15,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_run_order_decoding(tmp_path):
     exe = tmp_path / "run_order_check"
     subprocess.run(["g++", "-std=c++17", "-O1", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
-                    "-I" + os.path.join(ROOT, "paper_2305_06942_amd", "csrc"),
+                    "-I" + os.path.join(ROOT, "paper_2305_06942_amd", "csrc"), "-I" + os.path.join(ROOT, "include"),
                     os.path.join(ROOT, "tests", "run_order_check.cpp"), "-o", str(exe)], check=True)
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stdout + r.stderr

@@ -1,0 +1,99 @@
+"""The plan-free forward that allocates nothing (ebag_a2a_forward_noalloc),
+called through the C ABI, against the plan's forward (ebag_a2a_forward) on
+the same inputs: both run the same pooling kernel in the same order, so the
+send buffers must agree bit for bit, and the flags must equal the epoch.
+Each case makes two calls in a row on the device's one scratch array, the
+second with a smaller input (fewer tables, a smaller batch), so leftovers of
+the first call would show in the second.  The results are also checked
+against the oracle."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from synth import device as sdev
+from tests.gpu_util import check_full, flags_np, make_plan, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2305_06942_amd as ebag
+    ebag.load()
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _pair(base, rows, T1, B1, T2, B2):
+    big = synth.scaled(base, rows=rows, T=T1, B=B1, name=base.name + "_noalloc_a")
+    small = synth.scaled(base, rows=rows, T=T2, B=B2, name=base.name + "_noalloc_b")
+    return big, small
+
+
+CASES = {
+    # (first call, second call), plan options
+    "tiny": (_pair(synth.TINY, 10_000, 4, 256, 2, 64), {}),
+    "dlrm": (_pair(synth.DLRM, 4000, 70, 1024, 9, 512), {}),
+    "skewed_table_major": (_pair(synth.SKEWED, 3000, 16, 1024, 8, 512),
+                           {"stream_rows": 0, "table_major": 1, "slice_granule": 1}),
+    "mixed_weighted_persistent": (_pair(synth.MIXED, 3000, 12, 4096, 4, 2048),
+                                  {"persistent_wgs_per_cu": 2, "table_major": 2, "slice_granule": 1}),
+    "large_comm_aware": (_pair(synth.LARGE, 3000, 16, 4096, 8, 2048), {"chunk_order": 1, "self_rank": 3}),
+    "mean": (_pair(synth.DLRM.with_(lengths="uniform:0:40"), 2000, 8, 1024, 3, 512), {"pooling_mode": 1}),
+}
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_noalloc_matches_plan_forward(name):
+    import torch
+    import paper_2305_06942_amd as ebag
+    (first, second), opts = CASES[name]
+    for call, w in enumerate((first, second)):
+        mean = opts.get("pooling_mode", 0) == 1
+        if mean:
+            w = w.with_(weighted=False)
+        say("noalloc", name, "call", call, "T", w.T, "B", w.B, "R", w.R, "C", w.C, opts)
+        inp = synth.make_inputs(w)
+        dev = sdev.to_device(inp)
+        n_flags = w.n_chunks * (w.T if opts.get("slice_granule", 0) == 1 else 1)
+        want = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+        got = torch.full_like(want, float("nan"))
+        f_want = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
+        f_got = torch.zeros_like(f_want)
+        plan = make_plan(w, **opts)
+        for epoch in (1, 2):
+            plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, want, f_want)
+            ebag.forward_noalloc(w.rows, w.dims, w.dtype, w.C, dev.tables, dev.indices, dev.offsets, dev.weights,
+                                 w.B, w.R, got, f_got, **opts)
+            torch.cuda.synchronize()
+            assert torch.equal(got.view(torch.int32), want.view(torch.int32)), "differs from the plan's forward"
+            assert np.all(flags_np(f_got) == epoch) and np.all(flags_np(f_want) == epoch)
+        plan.close()
+        if mean:
+            s64, a64, _ = oracle.pool_inputs(inp, mean=True)
+        else:
+            s64, a64, _ = oracle.pool_inputs(inp)
+        check_full(inp, got.cpu().numpy(), s64, a64)
+        want_flags = oracle.flags(w.B, w.R, w.C, 2, per_slice=w.T if opts.get("slice_granule", 0) == 1 else 1)
+        assert np.array_equal(flags_np(f_got), want_flags)
+
+
+def test_noalloc_integer_tables_bit_exact():
+    """Integer-valued tables have exactly one correct fp32 result."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    for w in (synth.TINY_INT, synth.scaled(synth.TINY_INT, rows=10_000, T=3, B=64, name="tiny_int_b")):
+        say("noalloc integer", w.T, w.B)
+        inp = synth.make_inputs(w)
+        dev = sdev.to_device(inp)
+        got = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+        flags = torch.zeros(w.n_chunks, dtype=torch.int32, device="cuda")
+        ebag.forward_noalloc(w.rows, w.dims, w.dtype, w.C, dev.tables, dev.indices, dev.offsets, dev.weights,
+                             w.B, w.R, got, flags)
+        torch.cuda.synchronize()
+        check_full(inp, got.cpu().numpy(), exact=True)
+        assert np.all(flags_np(flags) == 1)
