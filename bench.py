@@ -7,8 +7,10 @@ per-(destination, slice) ready flags.  Inputs are resident in HBM before the
 timed region.  Prints one JSON line (the headline workload, or one per
 workload with --all).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload dlrm]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--all] [--no-cpu-baseline] [--profile]
+       (no --workload: the large workload's line, with the other four
+       workloads' fused / unfused / consumer times and rooflines in it)
        python bench.py --summarize DIR     (rocprofv3 csv output -> text summary)
 """
 from __future__ import annotations
@@ -137,21 +139,6 @@ def time_each(fn, steps, stream):
         b.record(stream)
     torch.cuda.synchronize()
     return [a.elapsed_time(b) for a, b in ev]
-
-
-def hbm_probe(nbytes=4 << 30, reps=10):
-    """Achievable copy bandwidth (read + write bytes / time) with a 16-byte
-    vector copy kernel."""
-    import torch
-    from synth import device as sdev
-    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    src.fill_(1.0)
-    s = torch.cuda.current_stream()
-    sdev.copy(dst, src, nbytes)
-    ms = time_launches(lambda: sdev.copy(dst, src, nbytes), reps, s)
-    del src, dst
-    return 2 * nbytes / (ms * 1e-3) / 1e9, ms
 
 
 def gather_probe_gbs(row_bytes, nt=True, reps=5, buf_bytes=16 << 30, _cache={}):
@@ -401,7 +388,44 @@ def e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, consumer_first, p
     return round(1e3 * sorted(times)[len(times) // 2], 2) if times else None
 
 
-def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=False):
+ZIPF = ("skewed", "large")  # workloads whose rows repeat: HBM bytes are argued on counters and unique rows
+
+
+def roofline(name, alg, unique_bytes, fused_ms, traffic_bytes):
+    """Roofline of the fused pooling kernel for one workload.  frac: the
+    method's algorithmic bytes (every gathered row) over the kernel time, the
+    contract figure; under Zipf indices many rows hit L2 or the Infinity
+    Cache, so it can exceed the HBM peak.  frac_unique_rows: distinct rows
+    plus every other byte over the same time, the least HBM traffic the
+    launch can have.  frac_counter: the L2 fill and write bytes measured by
+    counters (FETCH_SIZE + WRITE_SIZE, an upper bound on HBM traffic, since
+    fills served by the Infinity Cache count too), null when the committed
+    counter record does not match the kernel sources.  claim names the
+    figure the workload's HBM efficiency is stated on."""
+    t = fused_ms * 1e-3
+    r = {"bound": "hbm", "achieved": round(alg / t / 1e9, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+         "frac": round(alg / t / 1e9 / HBM_PEAK_GBS, 4), "traffic": traffic_bytes,
+         "kernel": "fused_pool_kernel",
+         "frac_unique_rows": round(unique_bytes / t / 1e9 / HBM_PEAK_GBS, 4),
+         "frac_counter": None if traffic_bytes is None else round(traffic_bytes / t / 1e9 / HBM_PEAK_GBS, 4)}
+    if name in ZIPF:
+        r["claim"] = "frac_unique_rows"
+        r["basis"] = ("Zipf indices: rows repeat, so algorithmic bytes overstate HBM traffic; the claim is distinct "
+                      "rows + other bytes over the kernel time (a lower bound on HBM bytes), next to the counter "
+                      "bytes (an upper bound)")
+    else:
+        r["claim"] = "frac"
+        r["basis"] = ("uniform indices: a row's repeats are far apart in time, so every lookup is fetched past L2 "
+                      "(counter bytes match algorithmic bytes); distinct-row bytes are a looser lower bound")
+    return r
+
+
+def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=False, light=False, cpu_tables=None,
+                 queues=None):
+    """One workload's figures.  light: fused and unfused times, the
+    concurrent-consumer times and the roofline only (no per-launch timing,
+    trace, probes, CPU oracle or environment).  queues: a (producer,
+    consumer) pair of hardware-queue streams to reuse."""
     import dataclasses
 
     import numpy as np
@@ -451,7 +475,8 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
         unfused()
     unfused_ms = time_launches(unfused, steps, stream)
     # the same launches one at a time, for the median and the fastest
-    each = {} if profile else {"fused": time_each(fused, steps, stream), "unfused": time_each(unfused, steps, stream)}
+    each = {} if (profile or light) else {"fused": time_each(fused, steps, stream),
+                                          "unfused": time_each(unfused, steps, stream)}
     log(f"[{name}] fused {fused_ms * 1e3:.1f} us  unfused {unfused_ms * 1e3:.1f} us")
     assert np.all(flags.cpu().numpy().view(np.uint32) == epoch[0]), "flags do not match the number of forwards"
 
@@ -500,42 +525,85 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
     # End to end with the concurrent consumer: producer enqueued first, each
     # on a stream with a hardware queue of its own, so the two always run
     # concurrently.
-    prod, cons = ebag.queue_stream(), ebag.queue_stream()
+    own_queues = queues is None
+    prod, cons = (ebag.queue_stream(), ebag.queue_stream()) if own_queues else queues
     for fused_path in (True, False):
         key = ("fused" if fused_path else "unfused") + "_plus_consumer_us"
         out[key] = e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, False, prod, cons, stream, steps, warmup)
-    # overlap evidence from device timestamps
-    tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
-    e2e_us(tplan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, 0)
-    rel, drn, tpu = tplan.trace(n_flags)
-    tplan.close()
-    for q in (prod, cons):
-        ebag.queue_stream_destroy(q)
-    out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
-    out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
-    out["median_drain_lag_us"] = round(float(np.median(drn.astype(np.int64) - rel.astype(np.int64))) / tpu, 2)
-    out["n_slices"] = n_flags
+    if not light:
+        # overlap evidence from device timestamps
+        tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
+        e2e_us(tplan, w, dev, send, recv, flags, epoch, True, False, prod, cons, stream, 1, 0)
+        rel, drn, tpu = tplan.trace(n_flags)
+        tplan.close()
+        out["first_drain_before_last_release_us"] = round(float(int(rel.max()) - int(drn.min())) / tpu, 2)
+        out["slices_drained_before_last_release"] = int((drn < rel.max()).sum())
+        out["median_drain_lag_us"] = round(float(np.median(drn.astype(np.int64) - rel.astype(np.int64))) / tpu, 2)
+        out["n_slices"] = n_flags
+    if own_queues:
+        for q in (prod, cons):
+            ebag.queue_stream_destroy(q)
     rows_alg = int(sum(int(inp.lengths.reshape(w.T, w.B)[t].sum()) * w.dims[t] * w.elt for t in range(w.T)))
-    out["unique_row_gbs"] = round((alg - rows_alg + inp.unique_row_bytes()) / (fused_ms * 1e-3) / 1e9, 2)
-    probe, _ = hbm_probe()
-    out["hbm_copy_probe_gbs"] = round(probe, 1)
-    ceil_gbs, ceil_us = probe_ceiling(w, inp.lengths, inp.weights is not None, bool(opts.get("stream_rows", 1)))
-    out["random_row_probe_ceiling"] = {
-        "gbs": round(ceil_gbs, 1), "us": round(ceil_us, 1), "frac": round(out["value"] / ceil_gbs, 4),
-        "note": "uniform random rows of each table's width at the probe's measured rate; Zipf reuse can beat it"}
-    out["roofline"] = {"bound": "hbm", "achieved": out["value"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                       "frac": round(out["value"] / HBM_PEAK_GBS, 4), "traffic": None,
-                       "kernel": "fused_pool_kernel"}
+    unique_bytes = alg - rows_alg + inp.unique_row_bytes()
+    out["unique_row_bytes"] = unique_bytes
+    out["unique_row_gbs"] = round(unique_bytes / (fused_ms * 1e-3) / 1e9, 2)
+    if not light and name not in ZIPF:
+        ceil_gbs, ceil_us = probe_ceiling(w, inp.lengths, inp.weights is not None, bool(opts.get("stream_rows", 1)))
+        out["random_row_probe_ceiling"] = {
+            "gbs": round(ceil_gbs, 1), "us": round(ceil_us, 1), "frac": round(out["value"] / ceil_gbs, 4),
+            "note": "uniform random rows of each table's width at the probe's measured rate"}
     tr = None if (mean or per_table) else traffic_record(name)
-    if tr:
-        out["roofline"]["traffic"] = tr["hbm_bytes_per_launch"]
+    out["roofline"] = roofline(name, alg, unique_bytes, fused_ms, tr["hbm_bytes_per_launch"] if tr else None)
+    if light:
+        del dev, send, recv
+        return out
     out["paper_context"] = PAPER_CONTEXT
     del dev, send, recv
     torch.cuda.empty_cache()
     if with_cpu:
         log(f"[{name}] timing the CPU oracle")
-        out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes, mean=mean)
+        out["cpu_baseline"] = cpu_baseline(w, inp, algorithmic_bytes, max_tables=cpu_tables, mean=mean)
     out["env"] = env_info(inp)
+    return out
+
+
+# The headline line: the largest workload that fits one GPU (131 GB of tables
+# resident), many tables and long Zipf-distributed bags, the closest of the
+# five to the paper's many-table, long-pooling setting.
+HEADLINE = "large"
+# Tables the CPU oracle is timed on (all B samples of each), where the whole
+# workload would take too long or too much host memory.
+CPU_TABLES = {"large": 4}
+SECONDARY = ("tiny", "dlrm", "skewed", "mixed")
+_LIGHT_KEYS = ("fused_us", "unfused_us", "fused_speedup_vs_unfused", "fused_plus_consumer_us",
+               "unfused_plus_consumer_us", "pct_hbm_peak", "algorithmic_bytes", "unique_row_bytes", "plan_options")
+
+
+def run_headline(steps, warmup, with_cpu=True):
+    """The default line: the headline workload in full, and for each of the
+    other four its fused and unfused times, concurrent-consumer times and
+    roofline under "workloads" (no probes or CPU legs for those)."""
+    import paper_2305_06942_amd as ebag
+    import torch
+    queues = (ebag.queue_stream(), ebag.queue_stream())
+    try:
+        out = run_workload(HEADLINE, steps, warmup, with_cpu=with_cpu, profile=False,
+                           cpu_tables=CPU_TABLES.get(HEADLINE), queues=queues)
+        torch.cuda.empty_cache()
+        others = {}
+        for n in SECONDARY:
+            try:
+                r = run_workload(n, steps, warmup, with_cpu=False, profile=False, light=True, queues=queues)
+                others[n] = {k: r[k] for k in _LIGHT_KEYS if k in r}
+                others[n]["roofline"] = {k: r["roofline"][k] for k in
+                                         ("frac", "frac_unique_rows", "frac_counter", "traffic", "claim")}
+            except Exception as e:  # one failing workload must not lose the headline
+                others[n] = {"error": f"{type(e).__name__}: {e}"}
+            torch.cuda.empty_cache()
+        out["workloads"] = others
+    finally:
+        for q in queues:
+            ebag.queue_stream_destroy(q)
     return out
 
 
@@ -977,7 +1045,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="dlrm")
+    ap.add_argument("--workload", default=None,
+                    help="one workload (default: the large workload's line, with the other four in it)")
     ap.add_argument("--all", action="store_true", help="every workload, one JSON line each")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile", action="store_true", help="timing loops only (for rocprofv3 runs)")
@@ -1006,6 +1075,8 @@ def main():
             kernel, workload = ("backward_kernel" if a.backward else "fused_pool_kernel"), a.workload
         print(json.dumps(traffic(a.traffic[0], a.traffic[1], workload, kernel=kernel), indent=1))
         return 0
+    headline = a.workload is None
+    a.workload = a.workload or HEADLINE
     if a.gpus != 1:
         print(f"bench.py: the benchmark runs on one GPU; --gpus {a.gpus} is not supported (the R destinations "
               "are logical slices of one GPU's send buffer)", file=sys.stderr)
@@ -1048,10 +1119,14 @@ def main():
             return 2
         run_gemv_ar(a.steps, a.warmup, shapes=shapes, with_cpu=not (a.no_cpu_baseline or a.profile), profile=a.profile)
         return 0
+    if headline and not (a.all or a.profile or a.mean or a.per_table_slices):
+        print(json.dumps(run_headline(a.steps, a.warmup, with_cpu=not a.no_cpu_baseline)), flush=True)
+        return 0
     names = ["tiny", "dlrm", "skewed", "large", "mixed"] if a.all else [a.workload]
     for n in names:
         out = run_workload(n, a.steps, a.warmup, with_cpu=(not a.no_cpu_baseline and not a.profile), profile=a.profile,
-                           mean=a.mean, per_table=a.per_table_slices)
+                           mean=a.mean, per_table=a.per_table_slices,
+                           cpu_tables=CPU_TABLES.get(n))
         print(json.dumps(out), flush=True)
     return 0
 

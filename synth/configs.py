@@ -75,7 +75,8 @@ def _mk(name, cfg_id, T, rows, dims, dtype, B, R, C, lengths, indices, weighted,
     return Workload(name, cfg_id, T, r, d, dtype, B, R, C, lengths, indices, weighted, values)
 
 
-# The five workloads.  Index 1 ("dlrm") is the headline benchmark.
+# The five workloads.  The benchmark's headline line is "large", the largest
+# that fits one GPU (131 GB of tables); the other four are reported beside it.
 TINY = _mk("tiny", 0, 4, 10_000, [64], F32, 256, 2, 32, "fixed:8", "uniform", False, "normal")
 TINY_INT = TINY.with_(name="tiny_int", values="int8")
 DLRM = _mk("dlrm", 1, 32, 1_000_000, [128], F32, 4096, 8, 64, "fixed:32", "uniform", False, "uniform")

@@ -84,3 +84,18 @@ def test_summarize_keeps_the_dispatch_window(tmp_path):
     assert not any(l.startswith("B ") for l in out.splitlines())  # B has no dispatch 2
     full = bench.summarize(str(tmp_path / "t"))
     assert any(l.startswith("B ") and l.split()[1] == "1" for l in full.splitlines())
+
+
+def test_roofline_claims_and_fractions():
+    """Zipf workloads state their HBM efficiency on distinct-row bytes (with
+    the counter bytes beside them); uniform ones on algorithmic bytes."""
+    import bench
+    r = bench.roofline("large", alg=8_000_000_000, unique_bytes=4_000_000_000, fused_ms=1.0,
+                       traffic_bytes=6_000_000_000)
+    assert r["claim"] == "frac_unique_rows"
+    assert (r["frac"], r["frac_unique_rows"], r["frac_counter"]) == (1.0, 0.5, 0.75)
+    assert r["achieved"] == 8000.0 and r["peak"] == 8000.0 and r["traffic"] == 6_000_000_000
+    r = bench.roofline("dlrm", alg=4_000_000_000, unique_bytes=3_900_000_000, fused_ms=1.0, traffic_bytes=None)
+    assert r["claim"] == "frac" and r["frac"] == 0.5 and r["frac_counter"] is None
+    assert bench.HEADLINE == "large" and set(bench.SECONDARY) | {bench.HEADLINE} == {"tiny", "dlrm", "skewed",
+                                                                                      "large", "mixed"}
