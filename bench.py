@@ -47,20 +47,25 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    (table_major = 1, its hot rows fit an XCD's L2), large and mixed with
 #    one table at a time for the whole device (table_major = 2, the table's
 #    working set shares the device-wide cache);
+#  * the delivery stand-in that feeds the overlapped backward runs on a few
+#    multi-wave workgroups (library default 32 x 8 waves; large, whose
+#    backward runs longest, 16 x 16), so it holds few CUs;
 #  * there the consumer copies non-temporally (consume_nontemporal = 1), so
 #    its stream does not displace the producer's cached rows, with 1024-2048
 #    single-wave workgroups for the many short per-table items; dlrm streams
 #    its rows and keeps the defaults.
 PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1,
                         "backward_bags_per_run": 3},
-             "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1},
+             "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
+                       "deliver_wgs": 16, "deliver_waves_per_wg": 16},
              "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
                        "backward_bags_per_run": 8}}
 # Options that only steer the consumer (and, for the forward, the backward):
 # they do not change what a profiled kernel does.
 _NOT_FORWARD = {"consumer_wgs", "consume_nontemporal", "consume_timeout_us", "backward_bags_per_run",
-                "backward_waves_per_wg", "deliver_wgs"}
-_NOT_BACKWARD = {"consumer_wgs", "consume_nontemporal", "deliver_wgs", "stream_rows", "persistent_wgs_per_cu", "rows_in_flight",
+                "backward_waves_per_wg", "deliver_wgs", "deliver_waves_per_wg"}
+_NOT_BACKWARD = {"consumer_wgs", "consume_nontemporal", "deliver_wgs", "deliver_waves_per_wg", "stream_rows",
+                 "persistent_wgs_per_cu", "rows_in_flight",
                  "waves_per_wg", "bags_per_run", "check_indices", "release_mode"}
 
 
@@ -815,6 +820,11 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
         return None
     epoch = [0]
     send_q, bwd_q = ebag.queue_stream(), ebag.queue_stream()
+    # The bulk-synchronous sequence waits for the whole delivery, so it gets
+    # the fastest one: a bandwidth-sized copy of 2048 single-wave workgroups.
+    # The overlapped sequence uses the plan's delivery, which holds few CUs
+    # while the backward runs beside it.
+    bulk = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **dict(opts, deliver_wgs=2048, deliver_waves_per_wg=1))
 
     def sequence(fused):
         ev0, ev1, ev2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
@@ -825,7 +835,7 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
             bwd_q.wait_event(ev0)
             epoch[0] += 1
             with torch.cuda.stream(send_q):
-                plan.deliver(grad_dp, grad_recv, flags, w.B, w.R)
+                (plan if fused else bulk).deliver(grad_dp, grad_recv, flags, w.B, w.R)
             if not fused:
                 bwd_q.wait_stream(send_q)
             with torch.cuda.stream(bwd_q):
@@ -854,6 +864,7 @@ def run_backward(name, steps, warmup, profile=False, with_cpu=True):
     row["env"] = env_info(inp)
     print(json.dumps(row), flush=True)
     plan.close()
+    bulk.close()
     for q in (send_q, bwd_q):
         ebag.queue_stream_destroy(q)
     return row

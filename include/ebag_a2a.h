@@ -129,8 +129,11 @@ typedef struct ebag_a2a_opts {
                                   stream does not displace the producer's cached table rows (pays off
                                   when rows are reused: Zipf indices, small tables); 0 (default): plain
                                   loads and stores, which may hit the freshly written slices in cache */
-  int32_t deliver_wgs;         /* ebag_a2a_deliver: single-wave workgroups of the delivery stand-in, a copy
-                                  that never waits, sized to keep the memory system busy (default 2048) */
+  int32_t deliver_wgs;         /* ebag_a2a_deliver: workgroups of the delivery stand-in, a copy that never
+                                  waits (default 32) */
+  int32_t deliver_waves_per_wg; /* ebag_a2a_deliver: wavefronts per delivery workgroup, 1..16 (default 8);
+                                   each keeps eight 16-byte loads in flight per lane, so a few workgroups
+                                   feed the backward while holding only a few CUs */
 } ebag_a2a_opts_t;
 
 /* Fill *opts with the defaults listed above.  Returns EBAG_OK or EBAG_EINVAL. */
@@ -277,7 +280,7 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
  * ebag_a2a_backward from a second stream: on one GPU it plays the gradient
  * All-to-All whose arrival the backward overlaps (Sec. IV-D), the receiving
  * side of the flags of Sec. III-A.  Grid: the plan's deliver_wgs
- * single-wavefront workgroups.  Errors: EBAG_EINVAL for a null plan, buffer
+ * workgroups of deliver_waves_per_wg wavefronts.  Errors: EBAG_EINVAL for a null plan, buffer
  * or flags, misaligned buffers or a bad B / R split, checked before anything
  * is enqueued.
  */

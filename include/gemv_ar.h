@@ -58,18 +58,19 @@ extern "C" {
 typedef struct gemv_ar_plan* gemv_ar_t;
 
 typedef struct gemv_ar_opts {
-  int32_t tile_rows;           /* rows per output tile, 1..4096; 0 (default): 128, halved down to 32 while
-                                  the R ranks have fewer than 1024 tiles in all */
+  int32_t tile_rows;           /* rows per output tile, 1..4096; 0 (default): 128, halved down to 64 while
+                                  the R ranks have fewer than 2048 tiles in all */
   int32_t wgs_per_rank;        /* physical workgroups per rank P, at most the number of tiles; 0 (default):
-                                  one per tile (reduce_mode 0) or as many as can be resident at once for
-                                  the whole grid (reduce_mode 1) */
+                                  ceil(1024 / R), i.e. about 1024 workgroups in all, each taking one or more
+                                  tiles (reduce_mode 0), or as many as can be resident at once for the
+                                  whole grid (reduce_mode 1) */
   int32_t waves_per_wg;        /* wavefronts per workgroup, 1..16 (default 2) */
   int32_t comm_aware;          /* 1 (default): tiles owned by other ranks first; 0: tile order */
   int32_t debug_suppress_flag; /* >= 0: never set this peer flag ((owner * R + rank) * P + p), for
                                   failure-path tests; -1 (default) off */
   int32_t reduce_mode;         /* 0 (default): the last of the R ranks' workgroups p to store its partials
                                   for an owner reduces that owner's tiles (arrival counter, no waiting,
-                                  normal launch, P defaults to one tile per workgroup; can be captured
+                                  normal launch; can be captured
                                   into a graph and replayed); 1: the owner's workgroup waits for the
                                   peer flags and reduces (the paper's scheme; cooperative launch, every
                                   workgroup resident; the flags carry a per-call epoch, so a forward on

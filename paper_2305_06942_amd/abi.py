@@ -40,6 +40,7 @@ class Opts(ctypes.Structure):
         ("table_major", ctypes.c_int32),
         ("consume_nontemporal", ctypes.c_int32),
         ("deliver_wgs", ctypes.c_int32),
+        ("deliver_waves_per_wg", ctypes.c_int32),
     ]
 
 

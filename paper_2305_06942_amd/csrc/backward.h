@@ -51,6 +51,6 @@ struct DeliverArgs {
 };
 
 hipError_t launch_backward(const BackwardArgs& a, int64_t* value_base, int block, size_t lds, hipStream_t stream);
-hipError_t launch_deliver(const DeliverArgs& a, int grid, hipStream_t stream);
+hipError_t launch_deliver(const DeliverArgs& a, int grid, int block, hipStream_t stream);
 
 }  // namespace ebag

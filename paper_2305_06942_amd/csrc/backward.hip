@@ -159,16 +159,23 @@ __global__ __launch_bounds__(1024) void backward_kernel(const BackwardArgs a) {
   }
 }
 
-// One-GPU stand-in for the gradient All-to-All's arrival: single-wave
-// workgroups copy work items (32 KiB pieces of a whole slice, or one
-// (slice, table) block per item with per-table slices) from src to dst in
-// slice order with device-scope stores; when the last piece of a slice is
-// stored, its flag is incremented.
-__global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
-  const int lane = threadIdx.x;
+// One-GPU stand-in for the gradient All-to-All's arrival: every wavefront
+// copies work items (32 KiB pieces of a whole slice, or one (slice, table)
+// block per item with per-table slices) from src to dst in slice order with
+// device-scope stores, eight 16-byte loads in flight per lane; when the last
+// piece of a slice is stored, its flag is incremented.  A few multi-wave
+// workgroups keep the copy on a few CUs, so the backward it feeds keeps its
+// occupancy everywhere else (a real arrival comes through the links and DMA
+// engines and holds no CU at all).
+constexpr int DU = 8;  // loads in flight per lane
+
+__global__ __launch_bounds__(1024) void deliver_kernel(const DeliverArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  const int64_t n_waves = (int64_t)gridDim.x * (blockDim.x >> 6);
   const int64_t per_slice = a.per_table ? a.T : a.pieces;
   const int64_t n_items = a.so.n_chunks * per_slice;
-  for (int64_t x = blockIdx.x; x < n_items; x += gridDim.x) {
+  for (int64_t x = __builtin_amdgcn_readfirstlane(wave); x < n_items; x += n_waves) {
     int64_t gs, p;
     if (a.per_table) {  // (slice, table) items in production order
       int32_t tp, unused;
@@ -184,16 +191,27 @@ __global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
       const int dim = __builtin_amdgcn_readfirstlane(a.meta[t].dim);
       const int col_off = __builtin_amdgcn_readfirstlane(a.meta[t].col_off);
       const int v4 = dim >> 2, ld4 = a.sum_dim >> 2;
+      const int n = a.C * v4;
       const int64_t base = g * a.chunk_floats + col_off;
       const float4* src = reinterpret_cast<const float4*>(a.src + base);
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
           a.dst + base, 0, ((a.C - 1) * a.sum_dim + dim) * 4, 0x00020000);
-      for (int e = lane; e < a.C * v4; e += 64) {
-        const int row = e / v4;
-        const int off = row * ld4 + (e - row * v4);
-        const float4 v = src[off];
-        const u4v u = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
-        __builtin_amdgcn_raw_buffer_store_b128(u, rs, off * 16, 0, 16);  // device-scope store
+      for (int e0 = 0; e0 < n; e0 += 64 * DU) {
+        float4 v[DU];
+        int off[DU];
+#pragma unroll
+        for (int u = 0; u < DU; ++u) {
+          const int e = e0 + u * 64 + lane;
+          const int row = e / v4;
+          off[u] = e < n ? row * ld4 + (e - row * v4) : -1;
+          v[u] = off[u] >= 0 ? src[off[u]] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < DU; ++u) {
+          const u4v w = {__float_as_uint(v[u].x), __float_as_uint(v[u].y), __float_as_uint(v[u].z),
+                         __float_as_uint(v[u].w)};
+          if (off[u] >= 0) __builtin_amdgcn_raw_buffer_store_b128(w, rs, off[u] * 16, 0, 16);  // device scope
+        }
       }
       wait_all_memory();
       if (lane == 0)
@@ -205,10 +223,20 @@ __global__ __launch_bounds__(64) void deliver_kernel(const DeliverArgs a) {
       const float4* src = reinterpret_cast<const float4*>(a.src + g * a.chunk_floats) + e0;
       float4* dst = reinterpret_cast<float4*>(a.dst + g * a.chunk_floats) + e0;
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(dst, 0, n * 16, 0x00020000);
-      for (int i = lane; i < n; i += 64) {
-        const float4 v = src[i];
-        const u4v u = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)};
-        __builtin_amdgcn_raw_buffer_store_b128(u, rs, i * 16, 0, 16);  // device-scope store
+      for (int i0 = 0; i0 < n; i0 += 64 * DU) {
+        float4 v[DU];
+#pragma unroll
+        for (int u = 0; u < DU; ++u) {
+          const int i = i0 + u * 64 + lane;
+          v[u] = i < n ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < DU; ++u) {
+          const int i = i0 + u * 64 + lane;
+          const u4v w = {__float_as_uint(v[u].x), __float_as_uint(v[u].y), __float_as_uint(v[u].z),
+                         __float_as_uint(v[u].w)};
+          if (i < n) __builtin_amdgcn_raw_buffer_store_b128(w, rs, i * 16, 0, 16);  // device scope
+        }
       }
       wait_all_memory();
       if (lane == 0 &&
@@ -231,8 +259,8 @@ hipError_t launch_backward(const BackwardArgs& a, int64_t* value_base, int block
   return hipGetLastError();
 }
 
-hipError_t launch_deliver(const DeliverArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL(deliver_kernel, dim3(grid), dim3(64), 0, stream, a);
+hipError_t launch_deliver(const DeliverArgs& a, int grid, int block, hipStream_t stream) {
+  hipLaunchKernelGGL(deliver_kernel, dim3(grid), dim3(block), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -454,10 +454,12 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   if (opts) o = *opts; else gemv_ar_default_opts(&o);
   if (o.tile_rows < 0 || o.tile_rows > 4096) return fail(EBAG_EINVAL, "tile_rows must be 0 (auto) or in [1, 4096]");
   if (o.tile_rows == 0) {
-    // 128-row tiles, halved (down to 32) until the R ranks' tiles give at
-    // least 1024 workgroups: enough to cover launch and tail on 256 CUs.
+    // 128-row tiles, halved (down to 64) until the R ranks hold at least
+    // 2048 tiles: with about 1024 workgroups (below), each then computes two
+    // or more tiles, and the reduction that follows its first tile overlaps
+    // the GEMV of its next one instead of all waiting at the kernel's end.
     o.tile_rows = 128;
-    while (o.tile_rows > 32 && (int64_t)R * ((M + o.tile_rows - 1) / o.tile_rows) < 1024) o.tile_rows /= 2;
+    while (o.tile_rows > 64 && (int64_t)R * ((M + o.tile_rows - 1) / o.tile_rows) < 2048) o.tile_rows /= 2;
   }
   if (o.waves_per_wg < 1 || o.waves_per_wg > 16) return fail(EBAG_EINVAL, "waves_per_wg must be in [1, 16]");
   if (o.wgs_per_rank < 0) return fail(EBAG_EINVAL, "wgs_per_rank must be >= 0");
@@ -501,8 +503,9 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   }
   h->resident = per_cu * h->num_cus;
   // Owner-waits mode needs every workgroup resident (cooperative launch);
-  // the last-arriver mode does not and defaults to one tile per workgroup.
-  int64_t P = o.wgs_per_rank > 0 ? o.wgs_per_rank : owner_mode ? h->resident / R : h->n_tiles;
+  // the last-arriver mode does not and defaults to about 1024 workgroups in
+  // all (at most one tile each): one resident wave on 256 CUs.
+  int64_t P = o.wgs_per_rank > 0 ? o.wgs_per_rank : owner_mode ? h->resident / R : (1024 + R - 1) / R;
   if (P > h->n_tiles) P = h->n_tiles;
   if (P * R > INT_MAX) P = INT_MAX / R;
   if (P < 1 || (owner_mode && P * R > h->resident)) {

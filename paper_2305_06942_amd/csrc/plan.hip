@@ -203,6 +203,8 @@ int ebag::check_opts(const ebag_a2a_opts_t& o) {
   if (o.backward_waves_per_wg < 1 || o.backward_waves_per_wg > 16)
     return fail(EBAG_EINVAL, "backward_waves_per_wg must be in [1, 16]");
   if (o.deliver_wgs < 1) return fail(EBAG_EINVAL, "deliver_wgs must be >= 1");
+  if (o.deliver_waves_per_wg < 1 || o.deliver_waves_per_wg > 16)
+    return fail(EBAG_EINVAL, "deliver_waves_per_wg must be in [1, 16]");
   return EBAG_OK;
 }
 
@@ -385,7 +387,8 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
   o->consume_timeout_us = 5000000;
   o->backward_bags_per_run = 4;
   o->backward_waves_per_wg = 16;
-  o->deliver_wgs = 2048;
+  o->deliver_wgs = 32;
+  o->deliver_waves_per_wg = 8;
   return EBAG_OK;
 }
 
@@ -677,9 +680,11 @@ int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags
   d.sum_dim = h->sum_dim;
   d.per_table = h->opts.slice_granule == 1;
   const int64_t items = so.n_chunks * (d.per_table ? h->T : d.pieces);
+  const int waves = h->opts.deliver_waves_per_wg;
   int64_t grid = h->opts.deliver_wgs;
-  if (grid > items) grid = items;
-  const hipError_t e = launch_deliver(d, (int)grid, stream);
+  if (grid > (items + waves - 1) / waves) grid = (items + waves - 1) / waves;
+  if (grid > INT_MAX) grid = INT_MAX;
+  const hipError_t e = launch_deliver(d, (int)grid, 64 * waves, stream);
   if (e != hipSuccess) return hip_fail(e, "launch deliver kernel");
   return EBAG_OK;
 }

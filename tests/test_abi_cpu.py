@@ -42,7 +42,7 @@ def test_default_opts(lib):
     o = ebag.default_opts()
     assert (o.waves_per_wg, o.rows_in_flight, o.debug_suppress_flag) == (4, 8, -1)
     assert (o.backward_bags_per_run, o.backward_waves_per_wg) == (4, 16)
-    assert (o.consumer_wgs, o.deliver_wgs) == (512, 2048)
+    assert (o.consumer_wgs, o.deliver_wgs, o.deliver_waves_per_wg) == (512, 32, 8)
 
 
 def _create(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, max_batch=256, max_ranks=2, opts=None):
@@ -79,7 +79,8 @@ def test_create_rejects(lib, kw, msg):
     ("chunk_order", 2, "chunk_order"), ("consumer_wgs", 0, "consumer_wgs"),
     ("backward_bags_per_run", 0, "backward_bags_per_run"), ("backward_waves_per_wg", 17, "backward_waves_per_wg"),
     ("table_major", 3, "table_major"), ("table_major", -1, "table_major"), ("consume_nontemporal", 3, "consume_nontemporal"),
-    ("deliver_wgs", 0, "deliver_wgs"),
+    ("deliver_wgs", 0, "deliver_wgs"), ("deliver_waves_per_wg", 0, "deliver_waves_per_wg"),
+    ("deliver_waves_per_wg", 17, "deliver_waves_per_wg"),
 ])
 def test_create_rejects_opts(lib, field, value, msg):
     import paper_2305_06942_amd as ebag
