@@ -47,6 +47,8 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    (table_major = 1, its hot rows fit an XCD's L2), large and mixed with
 #    one table at a time for the whole device (table_major = 2, the table's
 #    working set shares the device-wide cache);
+#  * launch shapes from a sweep in each workload's order: skewed pools with 2
+#    wavefronts x 8 bags per workgroup, large with 8 bags per run;
 #  * the delivery stand-in that feeds the overlapped backward runs on a few
 #    multi-wave workgroups (library default 32 x 8 waves; large, whose
 #    backward runs longest, 16 x 16), so it holds few CUs;
@@ -55,9 +57,9 @@ TRAFFIC_FILE = {"fused_pool_kernel": "traffic_{}.json", "backward_kernel": "traf
 #    single-wave workgroups for the many short per-table items; dlrm streams
 #    its rows and keeps the defaults.
 PLAN_OPTS = {"skewed": {"stream_rows": 0, "table_major": 1, "slice_granule": 1, "consume_nontemporal": 1,
-                        "backward_bags_per_run": 3},
+                        "waves_per_wg": 2, "bags_per_run": 8, "backward_bags_per_run": 3},
              "large": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
-                       "deliver_wgs": 16, "deliver_waves_per_wg": 16},
+                       "bags_per_run": 8, "deliver_wgs": 16, "deliver_waves_per_wg": 16},
              "mixed": {"stream_rows": 0, "table_major": 2, "slice_granule": 1, "consume_nontemporal": 1,
                        "backward_bags_per_run": 8}}
 # Options that only steer the consumer (and, for the forward, the backward):

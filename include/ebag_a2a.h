@@ -53,6 +53,11 @@
  *  device work is enqueued on the given HIP stream; calls return as soon as
  *  the work is enqueued.  One forward (fused or unfused) may be in flight per
  *  plan at a time: the plan's slice counters and unfused scratch are shared.
+ *  Forwards on one stream are ordered; a forward enqueued on another stream
+ *  while the plan's last forward has not completed returns EBAG_EBUSY and
+ *  enqueues nothing (checked with an event; not checked under graph
+ *  capture).  Changed table pointers are uploaded by small kernels on the
+ *  forward's stream: the call never waits for the device.
  *
  * Errors: every entry point returns EBAG_OK (0) or a negative code, checked
  * before anything is enqueued; ebag_a2a_last_error() returns a message for
@@ -83,7 +88,7 @@ enum {
   EBAG_EHIP = -3,         /* a HIP runtime call failed */
   EBAG_ETIMEOUT = -4,     /* reported by ebag_a2a_status() */
   EBAG_ENOMEM = -5,       /* device or host allocation failed */
-  EBAG_EBUSY = -6         /* reserved */
+  EBAG_EBUSY = -6         /* a forward was enqueued on another stream while this plan's last one still runs */
 };
 
 /* Tuning and debugging knobs; pass NULL to ebag_a2a_create for defaults, or

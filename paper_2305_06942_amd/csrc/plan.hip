@@ -146,6 +146,11 @@ struct ebag_a2a_plan {
   std::vector<TabMeta> meta;
   std::vector<const void*> host_tables;  // last table pointers uploaded
   bool tables_valid = false;
+  // The last forward's completion, for refusing a forward on another stream
+  // while it still runs (the slice counters and scratch are shared).
+  hipEvent_t fwd_done = nullptr;
+  hipStream_t fwd_stream = nullptr;
+  bool fwd_pending = false;
   int64_t max_chunks = 0;
   int64_t max_flags = 0;   // max_chunks, times T with per-table slices
   // device memory
@@ -166,6 +171,7 @@ namespace {
 
 void free_plan(ebag_a2a_plan* h) {
   if (!h) return;
+  if (h->fwd_done) (void)hipEventDestroy(h->fwd_done);
   (void)hipFree(h->d_meta);
   (void)hipFree(h->d_tperm);
   (void)hipFree(h->d_tables);
@@ -251,17 +257,69 @@ int check_forward(const ebag_a2a_plan* h, const void* const* tables, const int32
   return EBAG_OK;
 }
 
-// Upload table pointers when they differ from the last upload.  The copy is
-// ordered on `stream` and completed before returning, so the caller's host
-// array may be reused immediately.
+constexpr int kPtrBatch = 64;
+struct PtrBatch {
+  const void** dst;
+  int32_t n;
+  int32_t pad;
+  const void* p[kPtrBatch];
+};
+
+// Writes n table pointers carried in the kernel arguments.
+__global__ __launch_bounds__(64) void put_pointers_kernel(const PtrBatch b) {
+  if ((int)threadIdx.x < b.n) b.dst[threadIdx.x] = b.p[threadIdx.x];
+}
+
+// Upload table pointers when they differ from the last upload: small
+// kernels ordered on `stream` that carry the pointers as arguments, so the
+// host neither waits nor keeps the array (it may be reused at once).
 int sync_tables(ebag_a2a_plan* h, const void* const* tables, hipStream_t stream) {
   if (h->tables_valid && std::memcmp(h->host_tables.data(), tables, sizeof(void*) * h->T) == 0) return EBAG_OK;
-  h->tables_valid = false;  // stays false unless this upload completes
+  h->tables_valid = false;  // stays false unless every upload is enqueued
+  for (int32_t first = 0; first < h->T; first += kPtrBatch) {
+    PtrBatch b;
+    std::memset(&b, 0, sizeof b);
+    b.dst = h->d_tables + first;
+    b.n = h->T - first < kPtrBatch ? h->T - first : kPtrBatch;
+    for (int32_t i = 0; i < b.n; ++i) b.p[i] = tables[first + i];
+    hipLaunchKernelGGL(put_pointers_kernel, dim3(1), dim3(64), 0, stream, b);
+    HIP_TRY(hipGetLastError(), "upload table pointers");
+  }
   std::memcpy(h->host_tables.data(), tables, sizeof(void*) * h->T);
-  HIP_TRY(hipMemcpyAsync(h->d_tables, h->host_tables.data(), sizeof(void*) * h->T, hipMemcpyHostToDevice, stream),
-          "upload table pointers");
-  HIP_TRY(hipStreamSynchronize(stream), "upload table pointers");
   h->tables_valid = true;
+  return EBAG_OK;
+}
+
+// Whether `stream` is being captured into a graph.  Work that waits for a
+// host-chosen epoch cannot be replayed from a graph: the epoch is fixed at
+// capture, so a replay would not wait for the flags of its own producer.
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
+// One forward in flight per plan: a forward on another stream than the last
+// one, while the last one has not completed, would share its counters.
+int check_busy(ebag_a2a_plan* h, hipStream_t stream) {
+  if (!h->fwd_pending || stream == h->fwd_stream || capturing(stream)) return EBAG_OK;
+  const hipError_t e = hipEventQuery(h->fwd_done);
+  if (e == hipErrorNotReady)
+    return fail(EBAG_EBUSY, "a forward of this plan is still running on another stream (the plan's slice counters "
+                            "and scratch are shared): order the forwards on one stream or wait for it");
+  if (e != hipSuccess) return hip_fail(e, "query the last forward");
+  h->fwd_pending = false;
+  return EBAG_OK;
+}
+
+// Remember the forward just enqueued on `stream` (not under graph capture).
+int note_forward(ebag_a2a_plan* h, hipStream_t stream) {
+  if (capturing(stream)) {
+    h->fwd_pending = false;
+    return EBAG_OK;
+  }
+  HIP_TRY(hipEventRecord(h->fwd_done, stream), "record the forward's completion");
+  h->fwd_stream = stream;
+  h->fwd_pending = true;
   return EBAG_OK;
 }
 
@@ -359,13 +417,7 @@ PoolSetup setup_of(const ebag_a2a_plan* h) {
 
 }  // namespace
 
-// Work that waits for a host-chosen epoch cannot be replayed from a graph:
-// the epoch is fixed at capture, so a replay would not wait for the flags of
-// its own producer.
-static bool capturing(hipStream_t stream) {
-  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-  return hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
-}
+
 
 extern "C" {
 
@@ -486,6 +538,7 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   CREATE_TRY(hipMemset(h->d_deliver_cnt, 0, sizeof(uint32_t) * h->max_chunks), "zero deliver counters");
   CREATE_TRY(hipMalloc((void**)&h->d_ticket, 2 * sizeof(uint32_t)), "alloc run ticket");
   CREATE_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
+  CREATE_TRY(hipEventCreateWithFlags(&h->fwd_done, hipEventDisableTiming), "create forward event");
   CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
   CREATE_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "init status");
   if (o.trace) {
@@ -506,17 +559,19 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   SliceOrder so;
   int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
-  rc = sync_tables(h, tables, stream);
+  rc = check_busy(h, stream);
   if (rc) return rc;
   PoolArgs a;
   fill_pool_args(setup_of(h), indices, offsets, weights, B, so, send_buf, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
   if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
+  rc = sync_tables(h, tables, stream);
+  if (rc) return rc;
   const int grid = pool_grid(setup_of(h), a.nruns, true, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(setup_of(h)), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
-  return EBAG_OK;
+  return note_forward(h, stream);
 }
 
 int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices,
@@ -525,12 +580,15 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   SliceOrder so;
   int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
-  rc = sync_tables(h, tables, stream);
+  rc = check_busy(h, stream);
   if (rc) return rc;
   PoolArgs a;
   fill_pool_args(setup_of(h), indices, offsets, weights, B, so, h->d_scratch, flags, &a);
   const int block = 64 * h->opts.waves_per_wg;
   if (a.nruns >= INT_MAX) return fail(EBAG_EINVAL, "too many runs (%lld) for one launch", (long long)a.nruns);
+  if (so.n_chunks * h->T > INT_MAX) return fail(EBAG_EINVAL, "too many slices x tables for the repack grid");
+  rc = sync_tables(h, tables, stream);
+  if (rc) return rc;
   const int grid = pool_grid(setup_of(h), a.nruns, false, weights != nullptr, block, a.out_floats);
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, false, needs_safe(setup_of(h)), a, grid,
                              block, stream);
@@ -557,7 +615,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   pa.suppress = h->opts.debug_suppress_flag;
   e = launch_publish(pa, stream);
   if (e != hipSuccess) return hip_fail(e, "launch flag publication kernel");
-  return EBAG_OK;
+  return note_forward(h, stream);
 }
 
 int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags, float* recv_buf, int64_t B,

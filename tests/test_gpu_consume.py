@@ -244,3 +244,36 @@ def test_stress_100_backward_epochs_across_flag_wraparound():
         torch.cuda.synchronize()
         assert torch.equal(values.view(torch.int32), want.view(torch.int32)), f"epoch {k}"
     assert plan.status_ex() == (0, -1, 0, -1)
+
+
+def test_overlapping_forwards_on_two_streams_refused():
+    """A forward enqueued on another stream while the plan's last forward has
+    not completed returns EBAG_EBUSY and enqueues nothing; on the same stream,
+    or once the last one completed, it runs.  The first forward is held back
+    by a bounded spin kernel queued ahead of it."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    if not hasattr(torch.cuda, "_sleep"):
+        pytest.skip("torch.cuda._sleep is not available")
+    w = SMALL_MIXED
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    send, _, flags = new_buffers(w)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        torch.cuda._sleep(200_000_000)
+        run(plan, w, dev, send, flags)
+    for fused in (True, False):
+        with pytest.raises(ebag.EbagError) as e:
+            run(plan, w, dev, send, flags, fused=fused, stream=s2)
+        assert e.value.code == ebag.abi.EBAG_EBUSY
+    with torch.cuda.stream(s1):
+        run(plan, w, dev, send, flags)  # same stream: ordered after the first
+    torch.cuda.synchronize()
+    run(plan, w, dev, send, flags, stream=s2)  # the others have completed
+    torch.cuda.synchronize()
+    assert np.all(flags_np(flags) == 3)
+    s64, a64, _ = oracle.pool_inputs(inp)
+    check_full(inp, send.cpu().numpy(), s64, a64)
