@@ -1,7 +1,7 @@
 """The entry points under HIP graph capture: a forward, a backward or a GEMV +
 AllReduce captured once and replayed several times, with the program's own
 eager work and synchronizations between the replays, gives the eager result
-bit for bit on every replay.  Nothing they enqueue is a memset; slice and
+bit for bit on every replay, and the eager result itself matches the oracle.  Nothing they enqueue is a memset; slice and
 arrival counters and the persistent grid's ticket re-arm themselves, so a
 replay needs no host work, and epoch flags advance by one per replay.  Calls
 that wait for a host-chosen epoch (the consumer, the backward with flags,
@@ -9,9 +9,10 @@ GEMV + AllReduce in reduce_mode 1) refuse to be captured."""
 import numpy as np
 import pytest
 
+import oracle
 import synth
 from synth import device as sdev
-from tests.gpu_util import flags_np, make_plan, new_buffers, run, say
+from tests.gpu_util import check_full, flags_np, make_plan, new_buffers, run, say
 from tests.test_gpu_parity import SMALL
 
 pytestmark = pytest.mark.gpu
@@ -61,6 +62,7 @@ def test_forward_graph_replays(name, opts, fused):
     flags = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
     run(plan, w, dev, send, flags, fused=fused)  # eager: also uploads the table pointers
     torch.cuda.synchronize()
+    check_full(inp, send.cpu().numpy())
     want = send.cpu().numpy().view(np.uint32).copy()
     g = _capture(lambda: run(plan, w, dev, send, flags, fused=fused))
     assert np.all(flags_np(flags) == 1), "capture must not execute"
@@ -86,6 +88,8 @@ def test_backward_graph_replays():
     plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values)
     torch.cuda.synchronize()
     want = values.cpu().numpy().view(np.uint32).copy()
+    ref = oracle.backward(w.dims, inp.offsets, inp.weights, grad.cpu().numpy(), w.B, w.R)
+    assert np.array_equal(want, ref.view(np.uint32)), "eager backward differs from the oracle"
     g = _capture(lambda: plan.backward(grad, dev.offsets, dev.weights, w.B, w.R, values))
     for k in range(1, REPLAYS + 1):
         values.fill_(float("nan"))
@@ -109,6 +113,10 @@ def test_gemv_allreduce_graph_replays():
     h.forward(A, x, y, out_flags)
     torch.cuda.synchronize()
     want = [t.cpu().numpy().view(np.uint32).copy() for t in y]
+    y64, abs64, _ = oracle.gemv_ar([a.cpu().numpy() for a in A], [v.cpu().numpy() for v in x], synth.F16)
+    depth = 8 + max(-(-(K * 2 // 16) // 64) for K in Ks) + 6 + R
+    err = np.abs(want[0].view(np.float32).astype(np.float64) - y64)
+    assert np.all(err <= depth * 2.0 ** -24 * abs64 + 1e-30), "eager GEMV + AllReduce differs from the oracle"
     g = _capture(lambda: h.forward(A, x, y, out_flags))
     for k in range(1, REPLAYS + 1):
         for t in y:

@@ -97,3 +97,37 @@ def test_noalloc_integer_tables_bit_exact():
         torch.cuda.synchronize()
         check_full(inp, got.cpu().numpy(), exact=True)
         assert np.all(flags_np(flags) == 1)
+
+
+def test_noalloc_at_its_limits():
+    """The stated maxima: 1024 tables (16 install launches), then 65,536
+    flags (one-sample slices); each call against the plan's forward bit for
+    bit and against the oracle."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    cases = [
+        (synth.scaled(synth.TINY, rows=64, T=1024, B=64, R=2, C=32, name="noalloc_1024_tables").with_(dims=(16,) * 1024),
+         {}),
+        (synth.scaled(synth.TINY, rows=1000, T=1, B=65536, R=1, C=1, name="noalloc_65536_flags"), {}),
+        (synth.scaled(synth.TINY, rows=1000, T=2, B=32768, R=2, C=1, name="noalloc_65536_table_flags"),
+         {"slice_granule": 1}),
+    ]
+    for w, opts in cases:
+        n_flags = w.n_chunks * (w.T if opts.get("slice_granule", 0) == 1 else 1)
+        say("noalloc limits", w.name, "T", w.T, "B", w.B, "flags", n_flags)
+        assert n_flags <= ebag.abi.NOALLOC_MAX_FLAGS and w.T <= ebag.abi.NOALLOC_MAX_TABLES
+        inp = synth.make_inputs(w)
+        dev = sdev.to_device(inp)
+        want = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+        got = torch.full_like(want, float("nan"))
+        f_want = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
+        f_got = torch.zeros_like(f_want)
+        plan = make_plan(w, **opts)
+        plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, want, f_want)
+        ebag.forward_noalloc(w.rows, w.dims, w.dtype, w.C, dev.tables, dev.indices, dev.offsets, dev.weights,
+                             w.B, w.R, got, f_got, **opts)
+        torch.cuda.synchronize()
+        plan.close()
+        assert torch.equal(got.view(torch.int32), want.view(torch.int32)), "differs from the plan's forward"
+        assert np.all(flags_np(f_got) == 1) and np.all(flags_np(f_want) == 1)
+        check_full(inp, got.cpu().numpy())
