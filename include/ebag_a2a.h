@@ -192,7 +192,8 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
  * GPU the library runs on holds until the process ends.  Each call first
  * enqueues a small kernel (one per 64 tables) that writes the descriptors
  * into that array and clears the counters, ticket and status word, then the
- * pooling kernel; it calls no hipMalloc, hipFree or other allocating routine.
+ * pooling kernel; it calls no hipMalloc, hipFree or other allocating routine
+ * (its host-side descriptors live on the calling thread's stack, about 52 KB).
  *   num_tables: 1 .. EBAG_NOALLOC_MAX_TABLES.
  *   opts: NULL for the defaults; trace = 1 and check_indices = 1 are refused
  *     with EBAG_EUNSUPPORTED (their results are read through a plan);
