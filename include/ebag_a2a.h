@@ -55,8 +55,9 @@
  *  plan at a time: the plan's slice counters and unfused scratch are shared.
  *  Forwards on one stream are ordered; a forward enqueued on another stream
  *  while the plan's last forward has not completed returns EBAG_EBUSY and
- *  enqueues nothing (checked with an event; not checked under graph
- *  capture).  Changed table pointers are uploaded by small kernels on the
+ *  enqueues nothing (checked on the host with an event, so also when that
+ *  stream waits for the other one; not checked under graph capture).  Order a
+ *  plan's forwards on one stream, or let the last one complete first.  Changed table pointers are uploaded by small kernels on the
  *  forward's stream: the call never waits for the device.
  *
  * Errors: every entry point returns EBAG_OK (0) or a negative code, checked
