@@ -131,3 +131,37 @@ def test_noalloc_at_its_limits():
         assert torch.equal(got.view(torch.int32), want.view(torch.int32)), "differs from the plan's forward"
         assert np.all(flags_np(f_got) == 1) and np.all(flags_np(f_want) == 1)
         check_full(inp, got.cpu().numpy())
+
+
+def test_noalloc_headline_workload_full_size():
+    """The large workload at full size in the benchmark's launch options
+    (128 tables, per-table slices: 512 x 128 = 65,536 flags, the stated
+    maximum): the whole send buffer equals the plan's forward bit for bit,
+    every element is written, and sampled bags match the oracle."""
+    import torch
+    import bench
+    import paper_2305_06942_amd as ebag
+    from tests.gpu_util import check_sampled
+    w = synth.FULL["large"]
+    opts = {k: v for k, v in bench.PLAN_OPTS["large"].items() if not k.startswith(("consume", "deliver", "backward"))}
+    n_flags = w.n_chunks * w.T
+    assert n_flags == ebag.abi.NOALLOC_MAX_FLAGS and opts.get("slice_granule") == 1
+    say("noalloc full size large", opts)
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    want = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+    got = torch.full_like(want, float("nan"))
+    f_want = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
+    f_got = torch.zeros_like(f_want)
+    plan = make_plan(w, **opts)
+    plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, want, f_want)
+    ebag.forward_noalloc(w.rows, w.dims, w.dtype, w.C, dev.tables, dev.indices, dev.offsets, dev.weights,
+                         w.B, w.R, got, f_got, **opts)
+    torch.cuda.synchronize()
+    plan.close()
+    assert not torch.isnan(got).any().item(), "some output element was never written"
+    assert torch.equal(got.view(torch.int32), want.view(torch.int32)), "differs from the plan's forward"
+    assert np.all(flags_np(f_got) == 1)
+    say("noalloc full size large: checked", check_sampled(inp, got, n_bags=200), "bags")
+    del dev, want, got
+    torch.cuda.empty_cache()
