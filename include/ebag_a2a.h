@@ -295,7 +295,10 @@ int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags
                      hipStream_t stream);
 
 /*
- * Synchronise the device and read the plan's status word.
+ * Synchronise the plan's device and read the plan's status word.  This call,
+ * ebag_a2a_status_ex, ebag_a2a_reset, ebag_a2a_trace and ebag_a2a_occupancy
+ * make the plan's device current for their duration and then restore the
+ * caller's current device.
  *   timed_out: 1 if a consumer gave up waiting, else 0.
  *   first_missing_flag: lowest flag index a consumer timed out on, else -1.
  * Returns EBAG_OK, or EBAG_ETIMEOUT when timed_out is set.

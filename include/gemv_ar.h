@@ -108,9 +108,10 @@ int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, flo
 int gemv_ar_unfused_forward(gemv_ar_t h, const void* const* A, const void* const* x, float* const* y,
                             uint32_t* out_flags, hipStream_t stream);
 
-/* Synchronise and read the status: out[0] 1 if an owner timed out, out[1]
- * the lowest peer flag index it gave up on (-1 none).  Returns EBAG_OK or
- * EBAG_ETIMEOUT. */
+/* Synchronise the plan's device and read the status: out[0] 1 if an owner
+ * timed out, out[1] the lowest peer flag index it gave up on (-1 none).
+ * Returns EBAG_OK or EBAG_ETIMEOUT.  This call and gemv_ar_reset make the
+ * plan's device current for their duration and then restore the caller's. */
 int gemv_ar_status(gemv_ar_t h, int32_t out[2]);
 
 /* Clear the status word (after a timeout).  Synchronous. */

@@ -24,6 +24,7 @@
 #include <vector>
 
 #include "common.h"
+#include "device_guard.h"
 #include "gemv_ar.h"
 
 namespace ebag {
@@ -592,6 +593,8 @@ int gemv_ar_unfused_forward(gemv_ar_t h, const void* const* A, const void* const
 
 int gemv_ar_status(gemv_ar_t h, int32_t out[2]) {
   if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
+  const DeviceGuard dg(h->device);
+  if (dg.error() != hipSuccess) return hipf(dg.error(), "make the plan's device current");
   hipError_t e = hipDeviceSynchronize();
   if (e != hipSuccess) return hipf(e, "synchronize");
   int32_t s[2];
@@ -604,6 +607,8 @@ int gemv_ar_status(gemv_ar_t h, int32_t out[2]) {
 
 int gemv_ar_reset(gemv_ar_t h) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
+  const DeviceGuard dg(h->device);
+  if (dg.error() != hipSuccess) return hipf(dg.error(), "make the plan's device current");
   hipError_t e = hipDeviceSynchronize();
   if (e == hipSuccess) e = hipMemcpy(h->d_status, kGemvStatusInit, sizeof(kGemvStatusInit), hipMemcpyHostToDevice);
   if (e != hipSuccess) return hipf(e, "reset status");

@@ -14,6 +14,7 @@
 #include "table_order.h"
 #include "backward.h"
 #include "consume.h"
+#include "device_guard.h"
 
 using namespace ebag;
 
@@ -688,6 +689,8 @@ int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags
 
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]) {
   if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
+  const DeviceGuard dg(h->device);
+  HIP_TRY(dg.error(), "make the plan's device current");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   int32_t s[4];
   HIP_TRY(hipMemcpy(s, h->d_status, sizeof s, hipMemcpyDeviceToHost), "read status");
@@ -709,6 +712,8 @@ int ebag_a2a_status(ebag_a2a_t h, int32_t* timed_out, int32_t* first_missing_fla
 
 int ebag_a2a_reset(ebag_a2a_t h) {
   if (!h) return fail(EBAG_EINVAL, "null plan");
+  const DeviceGuard dg(h->device);
+  HIP_TRY(dg.error(), "make the plan's device current");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   HIP_TRY(hipMemset(h->d_counters, 0, sizeof(uint32_t) * h->max_flags), "zero counters");
   HIP_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
@@ -726,6 +731,8 @@ int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks,
   if (!h) return fail(EBAG_EINVAL, "null plan");
   if (!h->d_trace_release) return fail(EBAG_EINVAL, "plan was created without trace = 1");
   if (n < 0 || n > h->max_flags) return fail(EBAG_EINVAL, "n=%lld outside [0, %lld]", (long long)n, (long long)h->max_flags);
+  const DeviceGuard dg(h->device);
+  HIP_TRY(dg.error(), "make the plan's device current");
   HIP_TRY(hipDeviceSynchronize(), "synchronize");
   if (release_ticks && n)
     HIP_TRY(hipMemcpy(release_ticks, h->d_trace_release, sizeof(uint64_t) * n, hipMemcpyDeviceToHost), "read trace");
@@ -737,7 +744,8 @@ int ebag_a2a_trace(ebag_a2a_t h, uint64_t* release_ticks, uint64_t* drain_ticks,
 
 int ebag_a2a_occupancy(ebag_a2a_t h, int32_t weighted, int32_t out[4]) {
   if (!h || !out) return fail(EBAG_EINVAL, "null plan or output");
-  HIP_TRY(hipSetDevice(h->device), "set device");
+  const DeviceGuard dg(h->device);
+  HIP_TRY(dg.error(), "make the plan's device current");
   // Same launch shape as a forward: the LDS tile does not depend on B.
   PoolArgs a;
   SliceOrder so;
