@@ -156,6 +156,36 @@ def test_backward_fused_with_delivery(opts):
         _check(inp, grad_dp, values, bool(opts.get("pooling_mode")))
 
 
+@pytest.mark.parametrize("granule", [0, 1])
+@pytest.mark.parametrize("wgs,waves", [(1, 1), (1, 16), (3, 4), (32, 8), (16, 16), (2048, 1)])
+def test_delivery_shapes(wgs, waves, granule):
+    """The gradient's arrival stand-in over its launch shapes: one wavefront
+    doing every item, a few wide workgroups, more wavefronts than items.  Whole
+    slices here are 22.5 pieces of 32 KiB (a ragged last piece), so the
+    per-slice piece counter is exercised; per-table slices take one item per
+    (slice, table).  Two epochs, fused with the backward: the delivered
+    gradient equals its source bit for bit, every flag holds the epoch, the
+    piece counters re-arm, and the backward matches the oracle."""
+    import torch
+    inp = synth.make_inputs(SMALL["mixed_small"])
+    w = inp.w
+    assert (w.C * w.sum_dim) % 8192 != 0  # the last piece of a slice is ragged
+    dev = sdev.to_device(inp)
+    plan = make_plan(w, slice_granule=granule, table_major=granule, deliver_wgs=wgs, deliver_waves_per_wg=waves)
+    say("delivery shape", wgs, waves, granule)
+    flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
+    for epoch in (1, 2):
+        grad_dp = _grad(w, 300 + epoch)
+        grad_recv = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+        values = torch.full((_n_values(inp),), float("nan"), device="cuda")
+        _fused(plan, w, dev, grad_dp, grad_recv, flags, values, epoch)
+        assert plan.status_ex() == (0, -1, 0, -1)
+        assert np.all(flags.cpu().numpy() == epoch), f"epoch {epoch}: flags"
+        assert torch.equal(grad_dp.view(torch.int32), grad_recv.view(torch.int32)), f"epoch {epoch}: delivered gradient"
+        _check(inp, grad_dp, values, False)
+    plan.close()
+
+
 def test_backward_times_out_without_delivery():
     import torch
     w = SMALL["dlrm_small"]

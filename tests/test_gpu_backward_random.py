@@ -43,7 +43,9 @@ def test_random_backward(seed):
     opts = dict(pooling_mode=fopts["pooling_mode"], slice_granule=fopts["slice_granule"],
                 chunk_order=fopts["chunk_order"], self_rank=fopts["self_rank"], table_major=fopts["table_major"],
                 backward_bags_per_run=int(rng.choice([1, 2, 3, 7, 64])),
-                backward_waves_per_wg=int(rng.choice([1, 2, 8, 16])))
+                backward_waves_per_wg=int(rng.choice([1, 2, 8, 16])),
+                deliver_wgs=int(rng.choice([1, 3, 32, 2048])),
+                deliver_waves_per_wg=int(rng.choice([1, 4, 16])))
     say("random backward", seed, dict(T=w.T, dims=w.dims, B=w.B, R=w.R, C=w.C, nnz=inp.nnz), opts)
     plan = make_plan(w, **opts)
     offsets = torch.from_numpy(inp.offsets).cuda()
@@ -68,6 +70,9 @@ def test_random_backward(seed):
             plan.backward(g, offsets, weights, w.B, w.R, values)
         torch.cuda.synchronize()
         assert plan.status_ex() == (0, -1, 0, -1)
+        if fused:
+            assert np.all(flags.cpu().numpy() == 1), "delivery flags"
+            assert torch.equal(recv.view(torch.int32), g.view(torch.int32)), "delivered gradient"
         got = values.cpu().numpy()
         bad = np.flatnonzero(got[:n].view(np.uint32) != want.view(np.uint32))
         assert bad.size == 0, f"{'fused' if fused else 'bulk'}: {bad.size} values differ, first at {bad[0]}"
