@@ -667,6 +667,41 @@ def _setup(name):
     return w, inp, dev, send, flags
 
 
+def run_placement(name, steps, warmup, reps=3):
+    """Fused and unfused kernel time with the send buffer allocated before the
+    tables and with it allocated after them (the benchmark's own order), on
+    the same inputs in one process, alternating.  The kernels write the send
+    layout's row pieces at a stride of sum(D) floats; where the buffer's pages
+    land decides how those pieces fall on the memory channels."""
+    import torch
+    import synth
+    import paper_2305_06942_amd as ebag
+    from synth import device as sdev
+    w = synth.FULL[name]
+    inp = synth.make_inputs(w)
+    before = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
+    dev = sdev.to_device(inp)
+    after = torch.empty((w.B, w.sum_dim), dtype=torch.float32, device="cuda")
+    flags = torch.zeros(w.n_chunks * w.T, dtype=torch.int32, device="cuda")
+    plan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, **dict(PLAN_OPTS.get(name, {})))
+    s = torch.cuda.current_stream()
+    out = {"study": "send-buffer placement", "workload": name, "steps": steps, "warmup": warmup,
+           "plan_options": PLAN_OPTS.get(name, {}),
+           "send_before_tables": hex(before.data_ptr()), "send_after_tables": hex(after.data_ptr()),
+           "first_table": hex(dev.tables[0].data_ptr()),
+           "fused_us": {"before_tables": [], "after_tables": []},
+           "unfused_us": {"before_tables": [], "after_tables": []}}
+    for _ in range(reps):
+        for key, buf in (("before_tables", before), ("after_tables", after)):
+            for kind, call in (("fused_us", plan.forward), ("unfused_us", plan.unfused_forward)):
+                f = lambda: call(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, buf, flags)
+                for _ in range(warmup):
+                    f()
+                out[kind][key].append(round(time_launches(f, steps, s) * 1e3, 1))
+    plan.close()
+    return out
+
+
 def run_occupancy(name, steps, warmup):
     """Fused-kernel time versus the fraction of resident workgroup slots a
     persistent grid occupies (Sec. IV-C, Fig. 13), for 2, 4 and 8 waves per
@@ -1077,6 +1112,8 @@ def main():
     ap.add_argument("--backward-sweep", action="store_true", help="backward kernel time per launch shape")
     ap.add_argument("--stream-probe", action="store_true", help="streaming read and write ceilings")
     ap.add_argument("--torch-baseline", action="store_true", help="PyTorch's embedding_bag path, for comparison")
+    ap.add_argument("--placement", action="store_true",
+                    help="fused and unfused time with the send buffer allocated before vs after the tables")
     a = ap.parse_args()
     if a.summarize:
         print(summarize(a.summarize, a.dispatches))
@@ -1101,6 +1138,9 @@ def main():
     torch.cuda.set_device(0)
     if a.occupancy:
         run_occupancy(a.workload, a.steps, a.warmup)
+        return 0
+    if a.placement:
+        print(json.dumps(run_placement(a.workload, a.steps, a.warmup)), flush=True)
         return 0
     if a.timeline:
         run_timeline(a.workload, a.warmup)
