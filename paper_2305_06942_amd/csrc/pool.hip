@@ -26,9 +26,10 @@
 // Run order (run_at): by default runs are numbered slice-major (all runs of
 // slice 0, then slice 1 ...), tables fastest inside a slice, so slices
 // complete progressively and a consumer can drain them while later slices
-// are still being pooled.  Table-major order pools one table at a time per
-// XCD (its hot rows stay cached); with per-table slices those still complete
-// progressively.
+// are still being pooled.  Table-major order pools one table at a time, on
+// each XCD separately (table_major = 1: the table's hot rows stay in that
+// XCD's L2) or on the whole device (table_major = 2: the table shares the
+// Infinity Cache); with per-table slices those still complete progressively.
 #include "common.h"
 
 namespace ebag {
