@@ -58,6 +58,13 @@ __device__ __forceinline__ float h2f(uint32_t bits16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
 }
 
+// fp16 rows: every element goes through one fma(w, widen(h), acc), also
+// without weights.  There the caller's w is 1 for a row it loaded and 0 for a
+// slot it left empty (whose row bits are zero), a value the compiler cannot
+// fold, so it emits one mixed-precision FMA per element (the fp16 operand is
+// widened inside the instruction) instead of a convert and an add.  Since
+// 1 * x and 0 * (+0) are exact, the single rounding gives the bits acc + x and
+// acc + 0 would: the result does not change, only the instruction count.
 template <> struct Widen<EF16> {
   template <bool WT>
   static __device__ __forceinline__ void add(float* acc, const u4v& r, float w) {
@@ -65,8 +72,8 @@ template <> struct Widen<EF16> {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float lo = h2f(u[e] & 0xffffu), hi = h2f(u[e] >> 16);
-      acc[2 * e] = WT ? __builtin_fmaf(w, lo, acc[2 * e]) : acc[2 * e] + lo;
-      acc[2 * e + 1] = WT ? __builtin_fmaf(w, hi, acc[2 * e + 1]) : acc[2 * e + 1] + hi;
+      acc[2 * e] = __builtin_fmaf(w, lo, acc[2 * e]);
+      acc[2 * e + 1] = __builtin_fmaf(w, hi, acc[2 * e + 1]);
     }
   }
 };
