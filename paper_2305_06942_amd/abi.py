@@ -151,6 +151,40 @@ def _need(buf, nbytes: int, what: str):
         raise ValueError(f"{what} holds {buf.numel() * buf.element_size()} bytes, needs {nbytes}")
 
 
+F32 = ("float32",)
+I32 = ("int32",)
+I64 = ("int64",)
+FLAG_TYPES = ("int32", "uint32")
+
+
+def _is_tensor(x) -> bool:
+    return x is not None and not isinstance(x, int) and hasattr(x, "is_contiguous")
+
+
+def _validate(*specs):
+    """Every torch tensor handed to a kernel must be contiguous, of the
+    element type the C ABI reads and on the GPU.  specs: (tensor, name,
+    allowed dtype names or None, element bytes or None); None and raw integer
+    addresses are skipped (those are the caller's responsibility).  Layout and
+    type are checked for every tensor before the device of any."""
+    ts = [sp for sp in specs if _is_tensor(sp[0])]
+    for x, what, kinds, elt in ts:
+        if not x.is_contiguous():
+            raise ValueError(f"{what} must be contiguous")
+        name = str(x.dtype).replace("torch.", "")
+        if kinds is not None and name not in kinds:
+            raise ValueError(f"{what} must be {' or '.join(kinds)}, not {name}")
+        if elt is not None and x.element_size() != elt:
+            raise ValueError(f"{what} must have {elt}-byte elements, not {x.element_size()}-byte {name}")
+    for x, what, _, _ in ts:
+        if x.device.type != "cuda":
+            raise ValueError(f"{what} must be a GPU tensor, not one on {x.device}")
+
+
+def _elt(dtype) -> int:
+    return 4 if int(dtype) == EBAG_F32 else 2
+
+
 def queue_stream():
     """A torch stream on a hardware queue of its own (ebag_a2a_queue_stream_create)."""
     import torch
@@ -191,6 +225,9 @@ def forward_noalloc(rows, dims, dtype, chunk_samples, tables, indices, offsets, 
     _need(send, 4 * int(B) * sum(int(d) for d in dims), "send buffer")
     _need(flags, 4 * n_flags, "flags")
     _need(offsets, 8 * (T * int(B) + 1), "offsets")
+    _validate(*[(t, f"table {i}", None, _elt(dtype)) for i, t in enumerate(tables)],
+              (indices, "indices", I32, None), (offsets, "offsets", I64, None), (weights, "weights", F32, None),
+              (send, "send buffer", F32, None), (flags, "flags", FLAG_TYPES, None))
     if hasattr(indices, "numel") and indices.numel() == 0:
         raise ValueError("indices must have a device address: pass a one-element buffer when every bag is empty")
     rows_a = (ctypes.c_int64 * T)(*[int(r) for r in rows])
@@ -215,6 +252,7 @@ class Plan:
         self.T = len(rows)
         self.dims = [int(d) for d in dims]
         self.C = int(chunk_samples)
+        self.elt = _elt(dtype)
         self.opts = o
         rows_a = (ctypes.c_int64 * self.T)(*[int(r) for r in rows])
         dims_a = (ctypes.c_int32 * self.T)(*self.dims)
@@ -253,14 +291,23 @@ class Plan:
         _need(offsets, 8 * (self.T * int(B) + 1), "offsets")
         return _addr(offsets)
 
+    def _fwd_types(self, tables, indices, offsets, weights, send, flags):
+        _validate(*[(t, f"table {i}", None, self.elt) for i, t in enumerate(tables)],
+                  (indices, "indices", I32, None), (offsets, "offsets", I64, None), (weights, "weights", F32, None),
+                  (send, "send buffer", F32, None), (flags, "flags", FLAG_TYPES, None))
+
     def forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
+        _need(offsets, 8 * (self.T * int(B) + 1), "offsets")
+        self._fwd_types(tables, indices, offsets, weights, send, flags)
         _check(self._lib.ebag_a2a_forward(self._h, self._tables(tables), self._indices(indices),
                                           self._offsets(B, offsets), _addr(weights), int(B), int(R), _addr(send),
                                           _addr(flags), _stream(stream)))
 
     def unfused_forward(self, tables, indices, offsets, weights, B, R, send, flags, stream=None):
         self._fwd_sizes(B, send, flags)
+        _need(offsets, 8 * (self.T * int(B) + 1), "offsets")
+        self._fwd_types(tables, indices, offsets, weights, send, flags)
         _check(self._lib.ebag_a2a_unfused_forward(self._h, self._tables(tables), self._indices(indices),
                                                   self._offsets(B, offsets), _addr(weights), int(B), int(R),
                                                   _addr(send), _addr(flags), _stream(stream)))
@@ -268,11 +315,15 @@ class Plan:
     def consume(self, send, flags, recv, B, R, expected_epoch, stream=None):
         self._fwd_sizes(B, send, flags)
         _need(recv, 4 * int(B) * sum(self.dims), "recv buffer")
+        _validate((send, "send buffer", F32, None), (flags, "flags", FLAG_TYPES, None), (recv, "recv buffer", F32, None))
         _check(self._lib.ebag_a2a_consume(self._h, _addr(send), _addr(flags), _addr(recv), int(B), int(R),
                                           int(expected_epoch) & 0xFFFFFFFF, _stream(stream)))
 
     def backward(self, grad, offsets, weights, B, R, values, grad_flags=None, expected_epoch=0, stream=None):
         self._fwd_sizes(B, grad, grad_flags)
+        _need(offsets, 8 * (self.T * int(B) + 1), "offsets")
+        _validate((grad, "gradient", F32, None), (grad_flags, "gradient flags", FLAG_TYPES, None),
+                  (offsets, "offsets", I64, None), (weights, "weights", F32, None), (values, "values", F32, None))
         _check(self._lib.ebag_a2a_backward(self._h, _addr(grad), _addr(grad_flags), int(expected_epoch) & 0xFFFFFFFF,
                                            self._offsets(B, offsets), _addr(weights), int(B), int(R), _addr(values),
                                            _stream(stream)))
@@ -280,6 +331,8 @@ class Plan:
     def deliver(self, src, dst, flags, B, R, stream=None):
         self._fwd_sizes(B, src, flags)
         _need(dst, 4 * int(B) * sum(self.dims), "destination buffer")
+        _validate((src, "source buffer", F32, None), (dst, "destination buffer", F32, None),
+                  (flags, "flags", FLAG_TYPES, None))
         _check(self._lib.ebag_a2a_deliver(self._h, _addr(src), _addr(dst), _addr(flags), int(B), int(R),
                                           _stream(stream)))
 
@@ -345,6 +398,7 @@ class GemvAR:
                 raise TypeError(f"unknown option {k}")
             setattr(o, k, int(v))
         self.R, self.M, self.K = int(R), int(M), [int(k) for k in K]
+        self.elt = _elt(dtype)
         self.opts = o
         ks = (ctypes.c_int64 * len(self.K))(*self.K)
         h = ctypes.c_void_p()
@@ -355,6 +409,12 @@ class GemvAR:
     def _arrays(self, A, x, y):
         if not (len(A) == len(x) == len(y) == self.R):
             raise ValueError(f"expected {self.R} buffers each for A, x and y")
+        for r in range(self.R):
+            _need(A[r], self.M * self.K[r] * self.elt, f"A[{r}]")
+            _need(x[r], self.K[r] * self.elt, f"x[{r}]")
+        _validate(*[(A[r], f"A[{r}]", None, self.elt) for r in range(self.R)],
+                  *[(x[r], f"x[{r}]", None, self.elt) for r in range(self.R)],
+                  *[(y[r], f"y[{r}]", F32, None) for r in range(self.R)])
         arr = ctypes.c_void_p * self.R
         return arr(*[_addr(a) for a in A]), arr(*[_addr(v) for v in x]), arr(*[_addr(v) for v in y])
 
@@ -362,6 +422,7 @@ class GemvAR:
         for v in y:
             _need(v, 4 * self.M, "output vector")
         _need(out_flags, 4 * self.R * self.launch_info()[0], "out_flags")
+        _validate((out_flags, "out_flags", FLAG_TYPES, None))
 
     def forward(self, A, x, y, out_flags=None, stream=None):
         self._out_sizes(y, out_flags)

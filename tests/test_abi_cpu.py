@@ -146,7 +146,7 @@ class _NoCalls:
 def _sizing_plan(T=2, dims=(64, 32), C=8):
     import paper_2305_06942_amd as ebag
     p = object.__new__(ebag.Plan)
-    p.T, p.dims, p.C = T, list(dims), C
+    p.T, p.dims, p.C, p.elt = T, list(dims), C, 4
     p.opts = ebag.default_opts()
     p._h, p._lib, p._tab_cache, p._empty_idx = None, _NoCalls(), None, None
     return p
@@ -170,6 +170,67 @@ def test_binding_rejects_undersized_buffers(lib, short):
     if short != "send":
         with pytest.raises(ValueError, match=short):
             p.backward(send, offsets, None, B, R, torch.zeros(8), grad_flags=flags, stream=0)
+
+
+def _typed_args(p, B=32, bad=None):
+    """Forward arguments of the right sizes as CPU tensors, one of them made
+    wrong in layout or element type by `bad`."""
+    import torch
+    send = torch.zeros(B, sum(p.dims))
+    flags = torch.zeros(B // p.C, dtype=torch.int32)
+    offsets = torch.zeros(p.T * B + 1, dtype=torch.int64)
+    tables = [torch.zeros(16, d) for d in p.dims]
+    idx = torch.zeros(4, dtype=torch.int32)
+    wts = None
+    if bad == "send_strided":
+        send = torch.zeros(sum(p.dims), B).t()
+    elif bad == "send_f64":
+        send = send.double()
+    elif bad == "indices_i64":
+        idx = idx.long()
+    elif bad == "offsets_i32":
+        offsets = torch.zeros(2 * (p.T * B + 1), dtype=torch.int32)
+    elif bad == "weights_f16":
+        wts = torch.zeros(4, dtype=torch.float16)
+    elif bad == "flags_f32":
+        flags = torch.zeros(B // p.C)
+    elif bad == "table_f16":
+        tables[1] = torch.zeros(16, 2 * p.dims[1], dtype=torch.float16)
+    return tables, idx, offsets, wts, send, flags
+
+
+@pytest.mark.parametrize("bad,msg", [
+    ("send_strided", "send buffer must be contiguous"), ("send_f64", "send buffer must be float32"),
+    ("indices_i64", "indices must be int32"), ("offsets_i32", "offsets must be int64"),
+    ("weights_f16", "weights must be float32"), ("flags_f32", "flags must be int32 or uint32"),
+    ("table_f16", "table 1 must have 4-byte elements"), (None, "table 0 must be a GPU tensor")])
+def test_binding_rejects_wrong_layout_type_or_device(lib, bad, msg):
+    """Tensors reach a kernel only when contiguous, of the element type the
+    C ABI reads, and on the GPU: each wrong case is refused on the host
+    before any call (these CPU tensors of the right sizes fail on layout or
+    type first, and on the device last)."""
+    p = _sizing_plan()
+    tables, idx, offsets, wts, send, flags = _typed_args(p, bad=bad)
+    for call in (p.forward, p.unfused_forward):
+        with pytest.raises(ValueError, match=msg):
+            call(tables, idx, offsets, wts, 32, 2, send, flags, stream=0)
+
+
+def test_binding_rejects_wrong_backward_and_consumer_buffers(lib):
+    import torch
+    p = _sizing_plan()
+    B = 32
+    grad = torch.zeros(B, sum(p.dims))
+    offsets = torch.zeros(p.T * B + 1, dtype=torch.int64)
+    with pytest.raises(ValueError, match="values must be float32"):
+        p.backward(grad, offsets, None, B, 2, torch.zeros(8, dtype=torch.float64), stream=0)
+    with pytest.raises(ValueError, match="gradient must be contiguous"):
+        p.backward(torch.zeros(sum(p.dims), B).t(), offsets, None, B, 2, torch.zeros(8), stream=0)
+    flags = torch.zeros(B // p.C, dtype=torch.int32)
+    with pytest.raises(ValueError, match="recv buffer must be contiguous"):
+        p.consume(grad, flags, torch.zeros(sum(p.dims), B).t(), B, 2, 1, stream=0)
+    with pytest.raises(ValueError, match="destination buffer must be float32"):
+        p.deliver(grad, torch.zeros(B, sum(p.dims), dtype=torch.float64), flags, B, 2, stream=0)
 
 
 def _noalloc(lib, T=2, rows=(10, 10), dims=(64, 64), dtype=0, C=32, B=256, R=2, opts=None, null_send=False):
