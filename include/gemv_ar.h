@@ -86,9 +86,13 @@ int gemv_ar_default_opts(gemv_ar_opts_t* opts);
  * K[r] columns per rank (host array of R values, each > 0 with K[r] * elt a
  * multiple of 16, K[r] * elt at most 64 KiB), storage type dtype.  The plan
  * owns the reduction slots (R * M floats), the peer flags, the arrival
- * counters and a status word.  One forward may be in flight per plan.  The
- * forwards must be called with the plan's device current (EBAG_EINVAL
- * otherwise).
+ * counters and a status word.  One forward may be in flight per plan:
+ * forwards on one stream are ordered, and a forward (fused or not) enqueued
+ * on another stream while the plan's last forward has not completed returns
+ * EBAG_EBUSY and enqueues nothing.  The check is an event recorded after each
+ * forward and queried on the host, so it also refuses a second stream that
+ * waits for the first; it is skipped under graph capture.  The forwards must
+ * be called with the plan's device current (EBAG_EINVAL otherwise).
  */
 int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_dtype_t dtype,
                    const gemv_ar_opts_t* opts);

@@ -371,6 +371,11 @@ struct gemv_ar_plan {
   int32_t block = 0;
   int32_t resident = 0;  // workgroups the device holds at once for the fused kernel
   uint32_t epoch = 0;
+  // The last forward's completion, for refusing a forward on another stream
+  // while it still runs (the reduction slots and counters are shared).
+  hipEvent_t fwd_done = nullptr;
+  hipStream_t fwd_stream = nullptr;
+  bool fwd_pending = false;
   float* d_part = nullptr;
   uint32_t* d_peer = nullptr;
   uint32_t* d_cnt = nullptr;
@@ -383,6 +388,7 @@ const int32_t kGemvStatusInit[2] = {0, INT_MAX};
 
 void free_gemv(gemv_ar_plan* h) {
   if (!h) return;
+  if (h->fwd_done) (void)hipEventDestroy(h->fwd_done);
   (void)hipFree(h->d_part);
   (void)hipFree(h->d_peer);
   (void)hipFree(h->d_cnt);
@@ -393,6 +399,38 @@ void free_gemv(gemv_ar_plan* h) {
 int hipf(hipError_t e, const char* what) { return fail(EBAG_EHIP, "%s: %s", what, hipGetErrorString(e)); }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool capturing(hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
+}
+
+// One forward in flight per plan: a forward on another stream than the last
+// one, while the last one has not completed, would share its reduction slots
+// and arrival counters.
+int check_busy(gemv_ar_plan* h, hipStream_t stream) {
+  if (!h->fwd_pending || stream == h->fwd_stream || capturing(stream)) return EBAG_OK;
+  const hipError_t e = hipEventQuery(h->fwd_done);
+  if (e == hipErrorNotReady)
+    return fail(EBAG_EBUSY, "a forward of this plan is still running on another stream (the reduction slots and "
+                            "counters are shared): order the forwards on one stream or wait for it");
+  if (e != hipSuccess) return hipf(e, "query the last forward");
+  h->fwd_pending = false;
+  return EBAG_OK;
+}
+
+// Remember the forward just enqueued on `stream` (not under graph capture).
+int note_forward(gemv_ar_plan* h, hipStream_t stream) {
+  if (capturing(stream)) {
+    h->fwd_pending = false;
+    return EBAG_OK;
+  }
+  const hipError_t e = hipEventRecord(h->fwd_done, stream);
+  if (e != hipSuccess) return hipf(e, "record the forward's completion");
+  h->fwd_stream = stream;
+  h->fwd_pending = true;
+  return EBAG_OK;
+}
 
 int fill_args(gemv_ar_plan* h, const void* const* A, const void* const* x, float* const* y, uint32_t* out_flags,
               GemvArgs* a) {
@@ -532,6 +570,7 @@ int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_
   GEMV_TRY(hipMemset(h->d_cnt, 0, sizeof(uint32_t) * (size_t)R * P), "zero arrival counters");
   GEMV_TRY(hipMalloc((void**)&h->d_status, sizeof(kGemvStatusInit)), "alloc status");
   GEMV_TRY(hipMemcpy(h->d_status, kGemvStatusInit, sizeof(kGemvStatusInit), hipMemcpyHostToDevice), "init status");
+  GEMV_TRY(hipEventCreateWithFlags(&h->fwd_done, hipEventDisableTiming), "create forward event");
 #undef GEMV_TRY
   *out = h;
   clear_error();
@@ -543,13 +582,12 @@ int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, flo
   GemvArgs a;
   int rc = fill_args(h, A, x, y, out_flags, &a);
   if (rc) return rc;
-  if (h->opts.reduce_mode == 1) {
-    // The peer flags carry this call's epoch, fixed at capture: a graph
-    // replay would see the previous replay's flags and not wait.
-    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-    if (hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
-      return fail(EBAG_EUNSUPPORTED, "reduce_mode 1 cannot be captured into a graph (use reduce_mode 0)");
-  }
+  // The peer flags carry this call's epoch, fixed at capture: a graph replay
+  // would see the previous replay's flags and not wait.
+  if (h->opts.reduce_mode == 1 && capturing(stream))
+    return fail(EBAG_EUNSUPPORTED, "reduce_mode 1 cannot be captured into a graph (use reduce_mode 0)");
+  rc = check_busy(h, stream);
+  if (rc) return rc;
   // A fresh epoch per forward: peer flags of earlier forwards never match.
   // Epoch 0 is the value the flags start from, so it is skipped.
   if (++h->epoch == 0) ++h->epoch;
@@ -559,20 +597,22 @@ int gemv_ar_forward(gemv_ar_t h, const void* const* A, const void* const* x, flo
                        (size_t)h->max_x_bytes, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hipf(e, "launch the fused GEMV + AllReduce kernel");
-    return EBAG_OK;
+    return note_forward(h, stream);
   }
   void* args[] = {&a};
   const hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(fused_fn(h->dtype)),
                                                   dim3((unsigned)(h->R * h->P)), dim3(h->block), args,
                                                   (unsigned)h->max_x_bytes, stream);
   if (e != hipSuccess) return hipf(e, "cooperative launch of the fused GEMV + AllReduce kernel");
-  return EBAG_OK;
+  return note_forward(h, stream);
 }
 
 int gemv_ar_unfused_forward(gemv_ar_t h, const void* const* A, const void* const* x, float* const* y,
                             uint32_t* out_flags, hipStream_t stream) {
   GemvArgs a;
   int rc = fill_args(h, A, x, y, out_flags, &a);
+  if (rc) return rc;
+  rc = check_busy(h, stream);
   if (rc) return rc;
   const int64_t g1 = (int64_t)h->R * h->n_tiles;
   if (g1 > INT_MAX) return fail(EBAG_EINVAL, "too many tiles for one launch");
@@ -588,7 +628,7 @@ int gemv_ar_unfused_forward(gemv_ar_t h, const void* const* A, const void* const
     e = hipGetLastError();
     if (e != hipSuccess) return hipf(e, "launch flag kernel");
   }
-  return EBAG_OK;
+  return note_forward(h, stream);
 }
 
 int gemv_ar_status(gemv_ar_t h, int32_t out[2]) {

@@ -172,3 +172,46 @@ def test_gemv_ar_random(seed):
     if rng.random() < 0.3:
         opts["wgs_per_rank"] = int(rng.integers(1, 9))
     _run(R, M, Ks, dtype, seed=1000 + seed, integer=bool(rng.integers(0, 2)), **opts)
+
+
+def test_overlapping_forwards_on_two_streams_refused():
+    """A forward (fused or not) enqueued on another stream while the plan's
+    last forward has not completed returns EBAG_EBUSY and enqueues nothing;
+    on the same stream it runs, ordered after the first.  The first forward
+    is held back by a bounded spin kernel queued ahead of it; every output
+    and flag is then checked against the oracle and the two forwards."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    if not hasattr(torch.cuda, "_sleep"):
+        pytest.skip("torch.cuda._sleep is not available")
+    R, M, Ks, dtype = 4, 4096 + 37, [1024, 512, 2048, 256], synth.F16
+    A, x = _inputs(R, M, Ks, dtype, 77)
+    y64, abs64, _ = oracle.gemv_ar(A, x, dtype)
+    dA = [_to_dev(a, dtype) for a in A]
+    dx = [_to_dev(v, dtype) for v in x]
+    plan = ebag.GemvAR(R, M, Ks, dtype)
+    P = plan.launch_info()[0]
+    y = [torch.full((M,), float("nan"), device="cuda") for _ in range(R)]
+    flags = torch.zeros(R * P, dtype=torch.int32, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        torch.cuda._sleep(200_000_000)
+        plan.forward(dA, dx, y, flags)
+    for call in (plan.forward, plan.unfused_forward):
+        with pytest.raises(ebag.EbagError) as e:
+            call(dA, dx, y, flags, stream=s2)
+        assert e.value.code == ebag.abi.EBAG_EBUSY
+    with torch.cuda.stream(s1):
+        plan.unfused_forward(dA, dx, y, flags)  # same stream: ordered after the first
+    torch.cuda.synchronize()
+    assert np.all(flags.cpu().numpy() == 2), "two forwards ran, the refused ones enqueued nothing"
+    assert plan.status() == (0, -1)
+    bound = _depth(R, Ks, dtype) * 2.0 ** -24 * abs64 + 1e-30
+    for r in range(R):
+        err = np.abs(y[r].cpu().numpy().astype(np.float64) - y64)
+        assert np.all(err <= bound), f"rank {r}"
+    plan.forward(dA, dx, y, flags, stream=s2)  # the first has completed: another stream is accepted
+    torch.cuda.synchronize()
+    assert np.all(flags.cpu().numpy() == 3)
+    plan.close()
