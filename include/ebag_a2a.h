@@ -57,8 +57,12 @@
  *  while the plan's last forward has not completed returns EBAG_EBUSY and
  *  enqueues nothing (checked on the host with an event, so also when that
  *  stream waits for the other one; not checked under graph capture).  Order a
- *  plan's forwards on one stream, or let the last one complete first.  Changed table pointers are uploaded by small kernels on the
- *  forward's stream: the call never waits for the device.
+ *  plan's forwards on one stream, or let the last one complete first.  In
+ *  the same way one backward (the plan's table bases are shared) and one
+ *  delivery (its per-slice piece counters are shared) may be in flight per
+ *  plan; these two are not checked, so order each on one stream.  Changed
+ *  table pointers are uploaded by small kernels on the forward's stream: the
+ *  call never waits for the device.
  *
  * Errors: every entry point returns EBAG_OK (0) or a negative code, checked
  * before anything is enqueued; ebag_a2a_last_error() returns a message for
