@@ -57,10 +57,11 @@
  *  while the plan's last forward has not completed returns EBAG_EBUSY and
  *  enqueues nothing (checked on the host with an event, so also when that
  *  stream waits for the other one; not checked under graph capture).  Order a
- *  plan's forwards on one stream, or let the last one complete first.  In
- *  the same way one backward (the plan's table bases are shared) and one
- *  delivery (its per-slice piece counters are shared) may be in flight per
- *  plan; these two are not checked, so order each on one stream.  Changed
+ *  plan's forwards on one stream, or let the last one complete first.  The
+ *  same holds, and is checked the same way, for the backward (the plan's
+ *  table bases are shared) and for the delivery (its per-slice piece
+ *  counters are shared): one of each may be in flight per plan, while a
+ *  backward and a delivery are independent of each other.  Changed
  *  table pointers are uploaded by small kernels on the forward's stream: the
  *  call never waits for the device.
  *

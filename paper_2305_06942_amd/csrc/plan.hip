@@ -70,6 +70,14 @@ int32_t ebag::table_groups_for(const ebag_a2a_opts_t& o, int32_t T, int n_xcd) {
   return o.table_major == 2 ? 1 : o.table_major == 1 ? (T % n_xcd == 0 ? n_xcd : 1) : 0;
 }
 
+// One kind of call whose device state a plan shares between calls: the
+// event recorded after the last one and the stream it was enqueued on.
+struct InFlight {
+  hipEvent_t done = nullptr;
+  hipStream_t stream = nullptr;
+  bool pending = false;
+};
+
 struct ebag_a2a_plan {
   int device = 0;
   int32_t T = 0;
@@ -86,11 +94,11 @@ struct ebag_a2a_plan {
   std::vector<TabMeta> meta;
   std::vector<const void*> host_tables;  // last table pointers uploaded
   bool tables_valid = false;
-  // The last forward's completion, for refusing a forward on another stream
-  // while it still runs (the slice counters and scratch are shared).
-  hipEvent_t fwd_done = nullptr;
-  hipStream_t fwd_stream = nullptr;
-  bool fwd_pending = false;
+  // The last forward's, backward's and delivery's completion, for refusing
+  // another of the same kind on another stream while it still runs (the
+  // slice counters and scratch, the table bases and the piece counters are
+  // shared).
+  InFlight fwd, bwd, dlv;
   int64_t max_chunks = 0;
   int64_t max_flags = 0;   // max_chunks, times T with per-table slices
   // device memory
@@ -111,7 +119,8 @@ namespace {
 
 void free_plan(ebag_a2a_plan* h) {
   if (!h) return;
-  if (h->fwd_done) (void)hipEventDestroy(h->fwd_done);
+  for (InFlight* f : {&h->fwd, &h->bwd, &h->dlv})
+    if (f->done) (void)hipEventDestroy(f->done);
   (void)hipFree(h->d_meta);
   (void)hipFree(h->d_tperm);
   (void)hipFree(h->d_tables);
@@ -238,28 +247,29 @@ bool capturing(hipStream_t stream) {
   return hipStreamIsCapturing(stream, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone;
 }
 
-// One forward in flight per plan: a forward on another stream than the last
-// one, while the last one has not completed, would share its counters.
-int check_busy(ebag_a2a_plan* h, hipStream_t stream) {
-  if (!h->fwd_pending || stream == h->fwd_stream || capturing(stream)) return EBAG_OK;
-  const hipError_t e = hipEventQuery(h->fwd_done);
+// One call of each kind in flight per plan: a call on another stream than
+// the last one of its kind, while that one has not completed, would share its
+// device state.
+int check_busy(InFlight& f, hipStream_t stream, const char* what) {
+  if (!f.pending || stream == f.stream || capturing(stream)) return EBAG_OK;
+  const hipError_t e = hipEventQuery(f.done);
   if (e == hipErrorNotReady)
-    return fail(EBAG_EBUSY, "a forward of this plan is still running on another stream (the plan's slice counters "
-                            "and scratch are shared): order the forwards on one stream or wait for it");
-  if (e != hipSuccess) return hip_fail(e, "query the last forward");
-  h->fwd_pending = false;
+    return fail(EBAG_EBUSY, "a %s of this plan is still running on another stream (the plan's device state for it "
+                            "is shared): order them on one stream or wait for it", what);
+  if (e != hipSuccess) return hip_fail(e, "query the last call");
+  f.pending = false;
   return EBAG_OK;
 }
 
-// Remember the forward just enqueued on `stream` (not under graph capture).
-int note_forward(ebag_a2a_plan* h, hipStream_t stream) {
+// Remember the call just enqueued on `stream` (not under graph capture).
+int note_call(InFlight& f, hipStream_t stream) {
   if (capturing(stream)) {
-    h->fwd_pending = false;
+    f.pending = false;
     return EBAG_OK;
   }
-  HIP_TRY(hipEventRecord(h->fwd_done, stream), "record the forward's completion");
-  h->fwd_stream = stream;
-  h->fwd_pending = true;
+  HIP_TRY(hipEventRecord(f.done, stream), "record the call's completion");
+  f.stream = stream;
+  f.pending = true;
   return EBAG_OK;
 }
 
@@ -478,7 +488,8 @@ int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per
   CREATE_TRY(hipMemset(h->d_deliver_cnt, 0, sizeof(uint32_t) * h->max_chunks), "zero deliver counters");
   CREATE_TRY(hipMalloc((void**)&h->d_ticket, 2 * sizeof(uint32_t)), "alloc run ticket");
   CREATE_TRY(hipMemset(h->d_ticket, 0, 2 * sizeof(uint32_t)), "zero run ticket");
-  CREATE_TRY(hipEventCreateWithFlags(&h->fwd_done, hipEventDisableTiming), "create forward event");
+  for (InFlight* f : {&h->fwd, &h->bwd, &h->dlv})
+    CREATE_TRY(hipEventCreateWithFlags(&f->done, hipEventDisableTiming), "create completion event");
   CREATE_TRY(hipMalloc((void**)&h->d_status, sizeof(kStatusInit)), "alloc status");
   CREATE_TRY(hipMemcpy(h->d_status, kStatusInit, sizeof(kStatusInit), hipMemcpyHostToDevice), "init status");
   if (o.trace) {
@@ -499,7 +510,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   SliceOrder so;
   int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
-  rc = check_busy(h, stream);
+  rc = check_busy(h->fwd, stream, "forward");
   if (rc) return rc;
   PoolArgs a;
   fill_pool_args(setup_of(h), indices, offsets, weights, B, so, send_buf, flags, &a);
@@ -511,7 +522,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
   hipError_t e = launch_pool(h->dtype, h->opts.rows_in_flight, weights != nullptr, true, needs_safe(setup_of(h)), a, grid,
                              block, stream);
   if (e != hipSuccess) return hip_fail(e, "launch fused pooling kernel");
-  return note_forward(h, stream);
+  return note_call(h->fwd, stream);
 }
 
 int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int32_t* indices,
@@ -520,7 +531,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   SliceOrder so;
   int rc = check_forward(h, tables, indices, offsets, weights, B, R, send_buf, flags, &so);
   if (rc) return rc;
-  rc = check_busy(h, stream);
+  rc = check_busy(h->fwd, stream, "forward");
   if (rc) return rc;
   PoolArgs a;
   fill_pool_args(setup_of(h), indices, offsets, weights, B, so, h->d_scratch, flags, &a);
@@ -555,7 +566,7 @@ int ebag_a2a_unfused_forward(ebag_a2a_t h, const void* const* tables, const int3
   pa.suppress = h->opts.debug_suppress_flag;
   e = launch_publish(pa, stream);
   if (e != hipSuccess) return hip_fail(e, "launch flag publication kernel");
-  return note_forward(h, stream);
+  return note_call(h->fwd, stream);
 }
 
 int ebag_a2a_consume(ebag_a2a_t h, const float* send_buf, const uint32_t* flags, float* recv_buf, int64_t B,
@@ -647,9 +658,11 @@ int ebag_a2a_backward(ebag_a2a_t h, const float* grad_buf, const uint32_t* grad_
   a.per_table = h->opts.slice_granule == 1;
   a.mean = h->opts.pooling_mode == 1;
   a.epoch = expected_epoch;
+  rc = check_busy(h->bwd, stream, "backward");
+  if (rc) return rc;
   const hipError_t e = launch_backward(a, h->d_value_base, block, lds, stream);
   if (e != hipSuccess) return hip_fail(e, "launch backward kernels");
-  return EBAG_OK;
+  return note_call(h->bwd, stream);
 }
 
 int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags, int64_t B, int32_t R,
@@ -682,9 +695,11 @@ int ebag_a2a_deliver(ebag_a2a_t h, const float* src, float* dst, uint32_t* flags
   int64_t grid = h->opts.deliver_wgs;
   if (grid > (items + waves - 1) / waves) grid = (items + waves - 1) / waves;
   if (grid > INT_MAX) grid = INT_MAX;
+  rc = check_busy(h->dlv, stream, "delivery");
+  if (rc) return rc;
   const hipError_t e = launch_deliver(d, (int)grid, 64 * waves, stream);
   if (e != hipSuccess) return hip_fail(e, "launch deliver kernel");
-  return EBAG_OK;
+  return note_call(h->dlv, stream);
 }
 
 int ebag_a2a_status_ex(ebag_a2a_t h, int32_t out[4]) {

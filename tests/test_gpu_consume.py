@@ -274,3 +274,49 @@ def test_overlapping_forwards_on_two_streams_refused():
     assert np.all(flags_np(flags) == 3)
     s64, a64, _ = oracle.pool_inputs(inp)
     check_full(inp, send.cpu().numpy(), s64, a64)
+
+
+def test_overlapping_backwards_and_deliveries_on_two_streams_refused():
+    """Likewise for the backward (its table bases are shared) and the
+    delivery (its piece counters are shared): a second one on another stream
+    while the first is held back by a spin kernel returns EBAG_EBUSY and
+    enqueues nothing; a backward and a delivery on two streams are
+    independent and both run.  The results match the oracle bit for bit."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    if not hasattr(torch.cuda, "_sleep"):
+        pytest.skip("torch.cuda._sleep is not available")
+    w = SMALL_MIXED
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    plan = make_plan(w)
+    g = torch.randn((w.B, w.sum_dim), generator=torch.Generator(device="cuda").manual_seed(41), device="cuda")
+    want = oracle.backward(w.dims, inp.offsets, inp.weights, g.cpu().numpy(), w.B, w.R)
+    values = torch.full((want.size,), float("nan"), device="cuda")
+    recv = torch.full_like(g, float("nan"))
+    flags = torch.zeros(plan.n_flags(w.B), dtype=torch.int32, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s1):
+        torch.cuda._sleep(200_000_000)
+        plan.backward(g, dev.offsets, dev.weights, w.B, w.R, values)
+        plan.deliver(g, recv, flags, w.B, w.R)
+    with pytest.raises(ebag.EbagError) as e:
+        plan.backward(g, dev.offsets, dev.weights, w.B, w.R, values, stream=s2)
+    assert e.value.code == ebag.abi.EBAG_EBUSY
+    with pytest.raises(ebag.EbagError) as e:
+        plan.deliver(g, recv, flags, w.B, w.R, stream=s2)
+    assert e.value.code == ebag.abi.EBAG_EBUSY
+    torch.cuda.synchronize()
+    assert np.all(flags.cpu().numpy() == 1), "one delivery ran, the refused one enqueued nothing"
+    assert torch.equal(recv.view(torch.int32), g.view(torch.int32))
+    assert np.array_equal(values.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    # a delivery on one stream and a backward waiting for it on another: both run
+    values.fill_(float("nan"))
+    with torch.cuda.stream(s1):
+        plan.deliver(g, recv, flags, w.B, w.R)
+    with torch.cuda.stream(s2):
+        plan.backward(recv, dev.offsets, dev.weights, w.B, w.R, values, grad_flags=flags, expected_epoch=2)
+    torch.cuda.synchronize()
+    assert plan.status_ex() == (0, -1, 0, -1)
+    assert np.array_equal(values.cpu().numpy().view(np.uint32), want.view(np.uint32))
