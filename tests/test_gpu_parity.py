@@ -162,12 +162,50 @@ def test_edge_cases(name):
         assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1))
 
 
+# Full-size workloads whose tables fit comfortably in host memory are checked
+# element by element over the whole batch; for the large workload (131 GB of
+# tables) every element of the column stripes of its first and last four
+# tables is checked, next to the sampled bags of every table.
+FULL_HOST_TABLE_BYTES = 20 << 30
+
+
+def _full_oracle(inp):
+    """(column ranges, sum64, abs64) of the oracle over whole tables: every
+    table when they fit in host memory, else the first and last four."""
+    w = inp.w
+    if w.table_bytes() <= FULL_HOST_TABLE_BYTES:
+        s64, a64, _ = oracle.pool_inputs(inp, want_send=False)
+        return [((0, w.T), s64, a64)]
+    out = []
+    for t0, t1 in ((0, 4), (w.T - 4, w.T)):
+        B = w.B
+        lo, hi = int(inp.offsets[t0 * B]), int(inp.offsets[t1 * B])
+        s64, a64, _ = oracle.pool([inp.table(t) for t in range(t0, t1)], w.dtype, w.dims[t0:t1],
+                                  inp.indices[lo:hi], inp.offsets[t0 * B:t1 * B + 1] - lo,
+                                  None if inp.weights is None else inp.weights[lo:hi], B, w.R, w.C, want_send=False)
+        out.append(((t0, t1), s64, a64))
+    return out
+
+
+def _check_columns(inp, send_np, parts):
+    w = inp.w
+    for (t0, t1), s64, a64 in parts:
+        c0, c1 = w.col_off[t0], w.col_off[t1 - 1] + w.dims[t1 - 1]
+        got = send_np[:, c0:c1]
+        ok, err, bound = oracle.within_tolerance(got, s64, a64)
+        if not ok:
+            i = np.unravel_index(np.argmax(err - bound), err.shape)
+            raise AssertionError(f"tables {t0}..{t1 - 1}: outside tolerance at {i}: gpu={got[i]} oracle={s64[i]}")
+
+
 @pytest.mark.parametrize("name", ["tiny", "dlrm", "skewed", "mixed", "large"])
 def test_full_size_sampled(name):
     """Full workload sizes, in the launch configuration the benchmark times
-    (and in the default one where they differ): sampled bags element by
-    element against the oracle, every element written, every flag equal to
-    the epoch, fused and unfused."""
+    (and in the default one where they differ), fused and unfused: every
+    element written, every flag equal to the epoch, sampled bags of every
+    table element by element against the per-bag oracle, and every element
+    against the C oracle over whole tables (all of them where they fit in host
+    memory; the first and last four of the large workload)."""
     import torch
     import bench
     w = synth.FULL[name]
@@ -179,6 +217,7 @@ def test_full_size_sampled(name):
     if launches[0]:
         launches.append({})
     send, _, _ = new_buffers(w)
+    parts = None
     for opts in launches:
         plan = make_plan(w, **opts)
         per_slice = w.T if opts.get("slice_granule") == 1 else 1
@@ -192,10 +231,14 @@ def test_full_size_sampled(name):
             assert not torch.isnan(send).any().item(), "some output element was never written"
             assert np.array_equal(flags_np(flags), oracle.flags(w.B, w.R, w.C, 1, per_slice=per_slice))
             n = check_sampled(inp, send, n_bags=200)
-            say("full", name, "checked", n, "bags")
+            if parts is None:
+                say("full", name, "oracle over whole tables")
+                parts = _full_oracle(inp)
+            _check_columns(inp, send.cpu().numpy(), parts)
+            say("full", name, "checked", n, "sampled bags and", sum(p[1].size for p in parts), "elements")
         assert plan.status_ex() == (0, -1, 0, -1)
         plan.close()
-    del dev, send, flags
+    del dev, send, flags, parts
     torch.cuda.empty_cache()
 
 
