@@ -225,7 +225,8 @@ def test_backward_full_size_sampled(name):
     """Full workload sizes in the launch configuration the backward benchmark
     times (the workload's plan options without the row-cache and grid ones),
     fused with the delivery: sampled bags bit for bit against the per-bag
-    oracle, every flag, and no value left unwritten."""
+    oracle, every value bit for bit against the C oracle, every flag, and no
+    value left unwritten."""
     import torch
     import bench
     from oracle import sampled
@@ -254,5 +255,21 @@ def test_backward_full_size_sampled(name):
         o = sampled.backward_value_offset(inp, t, b)
         got = values[o:o + want.size].cpu().numpy()
         assert np.array_equal(got.view(np.uint32), want.reshape(-1).view(np.uint32)), f"bag (t={t}, b={b})"
+    # Every value, bit for bit, against the C oracle, a group of tables at a
+    # time (its gradient columns and its block of values).
+    B, base = w.B, 0
+    for t0 in range(0, w.T, 16):
+        t1 = min(t0 + 16, w.T)
+        lo, hi = int(inp.offsets[t0 * B]), int(inp.offsets[t1 * B])
+        c0, c1 = w.col_off[t0], w.col_off[t1 - 1] + w.dims[t1 - 1]
+        want = oracle.backward(w.dims[t0:t1], inp.offsets[t0 * B:t1 * B + 1] - lo,
+                               None if inp.weights is None else inp.weights[lo:hi],
+                               np.ascontiguousarray(g[:, c0:c1]), B, w.R)
+        got = values[base:base + want.size].cpu().numpy()
+        bad = np.flatnonzero(got.view(np.uint32) != want.view(np.uint32))
+        assert bad.size == 0, f"tables {t0}..{t1 - 1}: {bad.size} values differ, first at {base + bad[0]}"
+        base += want.size
+    assert base == n
+    say("backward full", name, "every value checked")
     del values, grad_recv
     torch.cuda.empty_cache()
