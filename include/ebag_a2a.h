@@ -85,6 +85,8 @@ extern "C" {
 
 typedef struct ebag_a2a_plan* ebag_a2a_t;
 
+/* Table storage types.  Entry points take them as int32_t, so that any
+ * other value is an argument error (EBAG_EINVAL), never undefined behaviour. */
 typedef enum { EBAG_F32 = 0, EBAG_F16 = 1, EBAG_BF16 = 2 } ebag_dtype_t;
 
 enum {
@@ -156,7 +158,8 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* opts);
  * with buffers and a stream of that device.
  *   rows_per_table[T], dim_per_table[T]: host arrays; rows >= 0 (< 2^31), D > 0,
  *     D * elt % 16 == 0.
- *   table_dtype: storage type shared by all tables; pooled output is fp32.
+ *   table_dtype: storage type shared by all tables (EBAG_F32, EBAG_F16 or
+ *     EBAG_BF16; anything else is EBAG_EINVAL); pooled output is fp32.
  *   chunk_samples (C): samples per slice, > 0; one slice (C * sum(D) fp32)
  *     must be below 2 GiB.
  *   max_batch: largest B any forward will use (sizes the slice counters and
@@ -166,7 +169,7 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* opts);
  * descriptors, status word, trace buffers; released by ebag_a2a_destroy.
  */
 int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per_table,
-                    const int32_t* dim_per_table, ebag_dtype_t table_dtype, int32_t chunk_samples,
+                    const int32_t* dim_per_table, int32_t table_dtype, int32_t chunk_samples,
                     int64_t max_batch, int32_t max_ranks, const ebag_a2a_opts_t* opts);
 
 /*
@@ -219,7 +222,7 @@ int ebag_a2a_forward(ebag_a2a_t h, const void* const* tables, const int32_t* ind
 #define EBAG_NOALLOC_MAX_FLAGS 65536
 #define EBAG_NOALLOC_SCRATCH_BYTES (320 * 1024)
 int ebag_a2a_forward_noalloc(int32_t num_tables, const int64_t* rows_per_table, const int32_t* dim_per_table,
-                             ebag_dtype_t table_dtype, int32_t chunk_samples, const ebag_a2a_opts_t* opts,
+                             int32_t table_dtype, int32_t chunk_samples, const ebag_a2a_opts_t* opts,
                              const void* const* tables, const int32_t* indices, const int64_t* offsets,
                              const float* weights, int64_t B, int32_t R, float* send_buf, uint32_t* flags,
                              hipStream_t stream);

@@ -84,7 +84,8 @@ int gemv_ar_default_opts(gemv_ar_opts_t* opts);
 /*
  * Create a plan on the current HIP device for R ranks (1..16), M outputs and
  * K[r] columns per rank (host array of R values, each > 0 with K[r] * elt a
- * multiple of 16, K[r] * elt at most 64 KiB), storage type dtype.  The plan
+ * multiple of 16, K[r] * elt at most 64 KiB), storage type dtype (EBAG_F32,
+ * EBAG_F16 or EBAG_BF16; anything else is EBAG_EINVAL).  The plan
  * owns the reduction slots (R * M floats), the peer flags, the arrival
  * counters and a status word.  One forward may be in flight per plan:
  * forwards on one stream are ordered, and a forward (fused or not) enqueued
@@ -94,7 +95,7 @@ int gemv_ar_default_opts(gemv_ar_opts_t* opts);
  * waits for the first; it is skipped under graph capture.  The forwards must
  * be called with the plan's device current (EBAG_EINVAL otherwise).
  */
-int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_dtype_t dtype,
+int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, int32_t dtype,
                    const gemv_ar_opts_t* opts);
 
 /* Fused forward: one launch (cooperative with reduce_mode 1) computing

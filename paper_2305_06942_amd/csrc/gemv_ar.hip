@@ -481,7 +481,7 @@ int gemv_ar_default_opts(gemv_ar_opts_t* o) {
   return EBAG_OK;
 }
 
-int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, ebag_dtype_t dtype,
+int gemv_ar_create(gemv_ar_t* out, int32_t R, int64_t M, const int64_t* K, int32_t dtype,
                    const gemv_ar_opts_t* opts) {
   if (!out) return fail(EBAG_EINVAL, "null output handle");
   *out = nullptr;

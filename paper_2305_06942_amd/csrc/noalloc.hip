@@ -111,7 +111,7 @@ int log2_vecs(int v) {
 using namespace ebag;
 
 extern "C" int ebag_a2a_forward_noalloc(int32_t num_tables, const int64_t* rows_per_table,
-                                        const int32_t* dim_per_table, ebag_dtype_t table_dtype,
+                                        const int32_t* dim_per_table, int32_t table_dtype,
                                         int32_t chunk_samples, const ebag_a2a_opts_t* opts,
                                         const void* const* tables, const int32_t* indices, const int64_t* offsets,
                                         const float* weights, int64_t B, int32_t R, float* send_buf,

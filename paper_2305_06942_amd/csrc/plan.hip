@@ -395,7 +395,7 @@ int ebag_a2a_default_opts(ebag_a2a_opts_t* o) {
 }
 
 int ebag_a2a_create(ebag_a2a_t* out, int32_t num_tables, const int64_t* rows_per_table,
-                    const int32_t* dim_per_table, ebag_dtype_t table_dtype, int32_t chunk_samples,
+                    const int32_t* dim_per_table, int32_t table_dtype, int32_t chunk_samples,
                     int64_t max_batch, int32_t max_ranks, const ebag_a2a_opts_t* opts) {
   if (!out) return fail(EBAG_EINVAL, "null output handle");
   *out = nullptr;
