@@ -67,11 +67,11 @@ _lib = None
 _P = ctypes.c_void_p
 _SIGS = {
     "ebag_a2a_default_opts": ([_P], ctypes.c_int),
-    "ebag_a2a_create": ([_P, ctypes.c_int32, _P, _P, ctypes.c_int, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P],
+    "ebag_a2a_create": ([_P, ctypes.c_int32, _P, _P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, _P],
                         ctypes.c_int),
     "ebag_a2a_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_unfused_forward": ([_P, _P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
-    "ebag_a2a_forward_noalloc": ([ctypes.c_int32, _P, _P, ctypes.c_int, ctypes.c_int32, _P, _P, _P, _P, _P,
+    "ebag_a2a_forward_noalloc": ([ctypes.c_int32, _P, _P, ctypes.c_int32, ctypes.c_int32, _P, _P, _P, _P, _P,
                                   ctypes.c_int64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "ebag_a2a_consume": ([_P, _P, _P, _P, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32, _P], ctypes.c_int),
     "ebag_a2a_backward": ([_P, _P, _P, ctypes.c_uint32, _P, _P, ctypes.c_int64, ctypes.c_int32, _P, _P], ctypes.c_int),
@@ -86,7 +86,7 @@ _SIGS = {
     "ebag_a2a_destroy": ([_P], None),
     "ebag_a2a_last_error": ([], ctypes.c_char_p),
     "gemv_ar_default_opts": ([_P], ctypes.c_int),
-    "gemv_ar_create": ([_P, ctypes.c_int32, ctypes.c_int64, _P, ctypes.c_int, _P], ctypes.c_int),
+    "gemv_ar_create": ([_P, ctypes.c_int32, ctypes.c_int64, _P, ctypes.c_int32, _P], ctypes.c_int),
     "gemv_ar_forward": ([_P, _P, _P, _P, _P, _P], ctypes.c_int),
     "gemv_ar_unfused_forward": ([_P, _P, _P, _P, _P, _P], ctypes.c_int),
     "gemv_ar_status": ([_P, _P], ctypes.c_int),
