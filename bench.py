@@ -534,9 +534,13 @@ def run_workload(name, steps, warmup, with_cpu, profile, mean=False, per_table=F
     # concurrently.
     own_queues = queues is None
     prod, cons = (ebag.queue_stream(), ebag.queue_stream()) if own_queues else queues
+    # Below 0.1 ms the launch and cross-queue latencies dominate each sample:
+    # take the median over more of them.
+    e2e_steps = steps if fused_ms >= 0.1 else max(steps, 200)
     for fused_path in (True, False):
         key = ("fused" if fused_path else "unfused") + "_plus_consumer_us"
-        out[key] = e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, False, prod, cons, stream, steps, warmup)
+        out[key] = e2e_us(plan, w, dev, send, recv, flags, epoch, fused_path, False, prod, cons, stream, e2e_steps,
+                          warmup)
     if not light:
         # overlap evidence from device timestamps
         tplan = ebag.Plan(w.rows, w.dims, w.dtype, w.C, w.B, w.R, trace=1, **opts)
