@@ -99,3 +99,14 @@ def test_roofline_claims_and_fractions():
     assert r["claim"] == "frac" and r["frac"] == 0.5 and r["frac_counter"] is None
     assert bench.HEADLINE == "large" and set(bench.SECONDARY) | {bench.HEADLINE} == {"tiny", "dlrm", "skewed",
                                                                                       "large", "mixed"}
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    """The benchmark runs on one GPU: --gpus N > 1 exits with status 2 and
+    says why, before touching a GPU."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, os.path.abspath(bench.__file__), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and "--gpus 2" in r.stderr
