@@ -3,6 +3,7 @@ arguments before touching the GPU (no GPU needed)."""
 import ctypes
 import os
 import re
+import shutil
 
 import pytest
 
@@ -268,3 +269,25 @@ def test_noalloc_rejects_before_touching_the_device(lib, kw, code, msg):
     rc = _noalloc(lib, **kw)
     assert rc == getattr(ebag.abi, code), (rc, ebag.last_error())
     assert msg in ebag.last_error(), ebag.last_error()
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None or not os.path.isdir("/opt/rocm/include"),
+                    reason="needs gcc and the HIP headers")
+def test_headers_are_c_and_the_readme_example_compiles(tmp_path):
+    """Both headers are plain C11 (no C++ constructs), and the README's call
+    sequence compiles against them with the declared signatures."""
+    import re
+    import subprocess
+    readme = open(os.path.join(ROOT, "README.md")).read()
+    code = re.search(r"```c\n(.*?)```", readme, re.S).group(1)
+    prog = ('#include "ebag_a2a.h"\n#include "gemv_ar.h"\n#include <hip/hip_runtime_api.h>\nint main(void) {\n'
+            "  int32_t T = 2; int64_t rows[2] = {10, 10}; int32_t dims[2] = {64, 64};\n"
+            "  int32_t C = 8; int64_t B = 64; int32_t R = 2;\n"
+            "  const void* tables[2] = {0, 0}; const int32_t* indices = 0; const int64_t* offsets = 0;\n"
+            "  float* send = 0; float* recv = 0; uint32_t* flags = 0;\n" + code + "  return 0;\n}\n")
+    src = tmp_path / "readme_example.c"
+    src.write_text(prog)
+    r = subprocess.run(["gcc", "-std=c11", "-fsyntax-only", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__",
+                        "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"), str(src)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
