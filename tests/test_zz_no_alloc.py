@@ -165,3 +165,52 @@ def test_noalloc_headline_workload_full_size():
     say("noalloc full size large: checked", check_sampled(inp, got, n_bags=200), "bags")
     del dev, want, got
     torch.cuda.empty_cache()
+
+
+def test_noalloc_graph_replays():
+    """Under HIP graph capture, one of the uses this entry point exists for:
+    captured once and replayed three times.  Between replays an eager
+    plan-free call on another input leaves its own state in the device's
+    scratch array, and eager work and synchronizations run too.  Every replay
+    re-installs its descriptors and clears the counters, so each gives the
+    plan's forward result bit for bit, and the flags advance by one per
+    replay (capture itself runs nothing)."""
+    import torch
+    import paper_2305_06942_amd as ebag
+    w = synth.scaled(synth.MIXED, rows=3000, T=12, B=2048, name="mixed_noalloc_graph")
+    other = synth.scaled(synth.DLRM, rows=2000, T=5, B=512, name="dlrm_noalloc_graph_other")
+    opts = {"table_major": 2, "slice_granule": 1}
+    say("noalloc graph", w.T, w.B, opts)
+    inp = synth.make_inputs(w)
+    dev = sdev.to_device(inp)
+    o_inp = synth.make_inputs(other)
+    o_dev = sdev.to_device(o_inp)
+    n_flags = w.n_chunks * w.T
+    want = torch.full((w.B, w.sum_dim), float("nan"), device="cuda")
+    f_want = torch.zeros(n_flags, dtype=torch.int32, device="cuda")
+    plan = make_plan(w, **opts)
+    plan.forward(dev.tables, dev.indices, dev.offsets, dev.weights, w.B, w.R, want, f_want)
+    torch.cuda.synchronize()
+    check_full(inp, want.cpu().numpy())
+    plan.close()
+    got = torch.full_like(want, float("nan"))
+    f_got = torch.zeros_like(f_want)
+    o_send = torch.empty((other.B, other.sum_dim), device="cuda")
+    o_flags = torch.zeros(other.n_chunks, dtype=torch.int32, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ebag.forward_noalloc(w.rows, w.dims, w.dtype, w.C, dev.tables, dev.indices, dev.offsets, dev.weights,
+                             w.B, w.R, got, f_got, **opts)
+    torch.cuda.synchronize()
+    assert np.all(flags_np(f_got) == 0), "capture must not execute"
+    for k in range(1, 4):
+        ebag.forward_noalloc(other.rows, other.dims, other.dtype, other.C, o_dev.tables, o_dev.indices,
+                             o_dev.offsets, o_dev.weights, other.B, other.R, o_send, o_flags)
+        torch.cuda.synchronize()
+        got.fill_(float("nan"))
+        g.replay()
+        (torch.randn(256, 256, device="cuda") @ torch.randn(256, 256, device="cuda")).sum().item()
+        torch.cuda.synchronize()
+        assert torch.equal(got.view(torch.int32), want.view(torch.int32)), f"replay {k}"
+        assert np.all(flags_np(f_got) == k), f"replay {k}"
+    assert np.all(flags_np(o_flags) == 3)
